@@ -1,0 +1,165 @@
+"""Seeded synthetic inputs for packed variable-length video-latent attention.
+
+This module holds no attention arithmetic. It only draws inputs: per-clip token
+counts from latent grids (frames x height x width patches, one clip = one
+sequence, Section III Observation 2), the pack order, and q/k/v/dout values.
+Both the HIP path and the float64 oracle consume what it returns.
+
+Value recipe: every tensor is float32 N(0, 1) from ``numpy.random.default_rng``,
+rounded to bfloat16 with round-to-nearest-even. The draw order is fixed:
+(1) clip lengths, (2) pack-order permutation, (3) q, k, v, dout.
+The paper's datasets (WebVid, Koala, internal Lynx) are not available; these
+shapes stand in for them.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+
+import numpy as np
+
+# Latent grids (frames, height, width) -> tokens, named after what they are.
+GRID_5x16x16 = 5 * 16 * 16        # 1,280
+GRID_9x24x32 = 9 * 24 * 32        # 6,912
+GRID_13x30x52 = 13 * 30 * 52      # 20,280
+
+
+@dataclasses.dataclass
+class Pack:
+    """A packed batch: tensors are bf16 bit patterns (uint16) laid out [T, H, D]."""
+    name: str
+    cu_seqlens: np.ndarray          # int32 [nseq + 1], cu[0] = 0
+    heads: int
+    head_dim: int
+    scale: float
+    q: np.ndarray | None = None     # uint16 [T, H, D]
+    k: np.ndarray | None = None
+    v: np.ndarray | None = None
+    dout: np.ndarray | None = None
+
+    @property
+    def nseq(self) -> int:
+        return int(self.cu_seqlens.shape[0] - 1)
+
+    @property
+    def total_tokens(self) -> int:
+        return int(self.cu_seqlens[-1])
+
+    @property
+    def lengths(self) -> np.ndarray:
+        return np.diff(self.cu_seqlens).astype(np.int64)
+
+    @property
+    def sum_sq_len(self) -> int:
+        return int(np.sum(self.lengths ** 2))
+
+    def f32(self, name: str) -> np.ndarray:
+        """The bf16 values of tensor ``name`` widened exactly to float32."""
+        return bf16_bits_to_f32(getattr(self, name))
+
+
+def f32_to_bf16_bits(x: np.ndarray, chunk: int = 1 << 24) -> np.ndarray:
+    """Round float32 to bfloat16 (round-to-nearest-even), returning uint16 bits.
+
+    Inputs are finite normal draws, so NaN handling is not needed.
+    """
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    flat = x.reshape(-1).view(np.uint32)
+    out = np.empty(flat.shape, dtype=np.uint16)
+    for s in range(0, flat.size, chunk):
+        u = flat[s:s + chunk].astype(np.uint64)
+        r = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+        out[s:s + chunk] = r.astype(np.uint16)
+    return out.reshape(x.shape)
+
+
+def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
+    """Exact widening of bfloat16 bit patterns to float32."""
+    b = np.ascontiguousarray(b, dtype=np.uint16)
+    return (b.astype(np.uint32) << 16).view(np.float32)
+
+
+def cu_from_lengths(lengths) -> np.ndarray:
+    lengths = np.asarray(lengths, dtype=np.int64)
+    cu = np.zeros(lengths.shape[0] + 1, dtype=np.int64)
+    np.cumsum(lengths, out=cu[1:])
+    if cu[-1] >= 2 ** 31:
+        raise ValueError("total tokens exceed int32")
+    return cu.astype(np.int32)
+
+
+def _draw_tensors(rng: np.random.Generator, shape, n: int = 4, chunk_rows: int = 4096):
+    """Draw n float32 N(0,1) tensors of ``shape`` in order, each rounded to bf16."""
+    outs = []
+    T = shape[0]
+    for _ in range(n):
+        t = np.empty(shape, dtype=np.uint16)
+        # One draw per tensor in row chunks: the stream is identical to a single
+        # standard_normal(shape) call because numpy fills C-order sequentially.
+        for r0 in range(0, T, chunk_rows):
+            r1 = min(T, r0 + chunk_rows)
+            t[r0:r1] = f32_to_bf16_bits(rng.standard_normal((r1 - r0,) + tuple(shape[1:]), dtype=np.float32))
+        outs.append(t)
+    return outs
+
+
+WORKLOADS = ("tiny", "uniform", "hetero", "long", "skew")
+
+DESCRIPTIONS = {
+    "tiny": "2 clips (4x8x8=256, 6x8x8=384 tokens), 2 heads x 64",
+    "uniform": "8 clips x 4,096 tokens (16x16x16), 24 heads x 128",
+    "hetero": "16 clips drawn from {5x16x16=1,280 p.5; 9x24x32=6,912 p.35; 13x30x52=20,280 p.15}, shuffled, 24 heads x 128",
+    "long": "1 clip of 75,600 tokens (21x45x80), 24 heads x 128",
+    "skew": "1 clip of 100,800 tokens (28x60x60) + 64 images of 1,024 tokens (1x32x32), shuffled, 40 heads x 128",
+}
+
+
+def workload_shape(name: str, seed: int = 0):
+    """Lengths, heads and head_dim of a named workload, consuming the rng like make_workload."""
+    rng = np.random.default_rng(seed)
+    if name == "tiny":
+        lengths, H, D = [4 * 8 * 8, 6 * 8 * 8], 2, 64
+    elif name == "uniform":
+        lengths, H, D = [16 * 16 * 16] * 8, 24, 128
+    elif name == "hetero":
+        grid = np.array([GRID_5x16x16, GRID_9x24x32, GRID_13x30x52])
+        idx = rng.choice(3, size=16, p=[0.5, 0.35, 0.15])
+        lengths = grid[idx][rng.permutation(16)].tolist()
+        H, D = 24, 128
+    elif name == "long":
+        lengths, H, D = [21 * 45 * 80], 24, 128
+    elif name == "skew":
+        base = np.array([28 * 60 * 60] + [1 * 32 * 32] * 64)
+        lengths = base[rng.permutation(base.shape[0])].tolist()
+        H, D = 40, 128
+    else:
+        raise KeyError(f"unknown workload {name!r}; known: {WORKLOADS}")
+    return rng, lengths, H, D
+
+
+def make_workload(name: str, seed: int = 0, tensors: bool = True) -> Pack:
+    """One of the five named workloads, drawn from ``seed``."""
+    rng, lengths, H, D = workload_shape(name, seed)
+    cu = cu_from_lengths(lengths)
+    pack = Pack(name=name, cu_seqlens=cu, heads=H, head_dim=D, scale=1.0 / math.sqrt(D))
+    if tensors:
+        pack.q, pack.k, pack.v, pack.dout = _draw_tensors(rng, (int(cu[-1]), H, D))
+    return pack
+
+
+def make_pack(lengths, heads: int, head_dim: int, seed: int = 0, scale: float | None = None,
+              name: str = "custom") -> Pack:
+    """A pack with explicit clip lengths (zero-length clips allowed), drawn from ``seed``."""
+    rng = np.random.default_rng(seed)
+    cu = cu_from_lengths(lengths)
+    sc = 1.0 / math.sqrt(head_dim) if scale is None else float(scale)
+    pack = Pack(name=name, cu_seqlens=cu, heads=heads, head_dim=head_dim, scale=sc)
+    pack.q, pack.k, pack.v, pack.dout = _draw_tensors(rng, (int(cu[-1]), heads, head_dim))
+    return pack
+
+
+def attention_flops(pack: Pack) -> dict:
+    """FLOP conventions for bidirectional attention over the pack (per sequence L^2 work)."""
+    base = pack.heads * pack.head_dim * pack.sum_sq_len
+    return {"fwd": 4 * base, "bwd": 10 * base, "fwd_bwd": 14 * base,
+            "no_recompute": 12 * base, "executed": 18 * base}

@@ -1,0 +1,421 @@
+"""Pins for the float64 oracle, checked against facts that do not come from it.
+
+Each pin comes from the mathematics of softmax attention (the paper prints no
+attention values): closed forms for degenerate clips, invariants of the
+softmax Jacobian, finite differences, an independent library routine (torch's
+scaled_dot_product_attention with autograd, float64 on the CPU) and a
+pure-Python brute force. ``test_mutants_are_caught`` plants one plausible
+mistake at a time in a copy of the oracle and checks that some pin fails.
+"""
+import math
+import types
+
+import numpy as np
+import pytest
+
+import oracle.varlen_attention as orc
+from paper_2607_01701_amd.workload import cu_from_lengths, make_pack
+
+
+def rand_pack(lengths, H, D, seed, dtype=np.float64):
+    rng = np.random.default_rng(seed)
+    T = int(sum(lengths))
+    cu = cu_from_lengths(lengths)
+    q, k, v, do = (rng.standard_normal((T, H, D)).astype(dtype) for _ in range(4))
+    return cu, q, k, v, do
+
+
+def rel(a, b):
+    den = max(float(np.max(np.abs(b))), 1e-300)
+    return float(np.max(np.abs(np.asarray(a) - np.asarray(b)))) / den
+
+
+# ---------------------------------------------------------------- closed forms
+
+def check_len1(mod):
+    """P1: a one-token clip attends only to itself."""
+    cu, q, k, v, do = rand_pack([1, 1], 2, 8, 1)
+    sc = 0.37
+    r = mod.attention(q, k, v, do, cu, sc)
+    ok = np.allclose(r["out"], v, rtol=0, atol=1e-15)
+    ok &= np.allclose(r["lse"].T, sc * np.sum(q * k, axis=2), rtol=0, atol=1e-14)
+    ok &= np.all(np.abs(r["dq"]) < 1e-15) and np.all(np.abs(r["dk"]) < 1e-15)
+    ok &= np.allclose(r["dv"], do, rtol=0, atol=1e-15)
+    return bool(ok)
+
+
+def check_equal_v(mod):
+    """P2: identical value rows give that row as output."""
+    cu, q, k, v, do = rand_pack([9, 4], 2, 8, 2)
+    for s in range(2):
+        a, b = cu[s], cu[s + 1]
+        v[a:b] = v[a]
+    r = mod.attention(q, k, v, do, cu, 0.5)
+    return bool(np.allclose(r["out"][:9], np.broadcast_to(v[0], (9, 2, 8)), atol=1e-13)
+                and np.allclose(r["out"][9:], np.broadcast_to(v[9], (4, 2, 8)), atol=1e-13))
+
+
+def check_equal_k(mod):
+    """P3: identical key rows give uniform weights: mean of V, lse = s*q.k + ln L, dq = 0."""
+    L = 11
+    cu, q, k, v, do = rand_pack([L], 2, 8, 3)
+    k[:] = k[0]
+    sc = 0.3
+    r = mod.attention(q, k, v, do, cu, sc)
+    ok = np.allclose(r["out"], np.broadcast_to(v.mean(axis=0), v.shape), atol=1e-13)
+    lse_ref = sc * np.einsum("thd,hd->ht", q, k[0]) + math.log(L)
+    ok &= np.allclose(r["lse"], lse_ref, atol=1e-13)
+    ok &= np.all(np.abs(r["dq"]) < 1e-12)
+    return bool(ok)
+
+
+def check_len2_by_hand(mod):
+    """P4: two tokens, D = 1: p = sigmoid(s00 - s01), all gradients in closed form."""
+    qv, kv, vv, dov = [0.7, -1.3], [0.4, 1.1], [2.0, -0.5], [0.3, 1.7]
+    sc = 0.9
+    q = np.array(qv).reshape(2, 1, 1)
+    k = np.array(kv).reshape(2, 1, 1)
+    v = np.array(vv).reshape(2, 1, 1)
+    do = np.array(dov).reshape(2, 1, 1)
+    r = mod.attention(q, k, v, do, np.array([0, 2]), sc)
+    ok = True
+    for i in range(2):
+        s0, s1 = sc * qv[i] * kv[0], sc * qv[i] * kv[1]
+        p0 = 1.0 / (1.0 + math.exp(-(s0 - s1)))
+        p1 = 1.0 - p0
+        o = p0 * vv[0] + p1 * vv[1]
+        lse = max(s0, s1) + math.log(math.exp(s0 - max(s0, s1)) + math.exp(s1 - max(s0, s1)))
+        # d<do, o>/dq_i = do_i * sc * p0 p1 (k0 - k1)(v0 - v1)
+        dq = dov[i] * sc * p0 * p1 * (kv[0] - kv[1]) * (vv[0] - vv[1])
+        ok &= abs(r["out"][i, 0, 0] - o) < 1e-14
+        ok &= abs(r["lse"][0, i] - lse) < 1e-14
+        ok &= abs(r["dq"][i, 0, 0] - dq) < 1e-14
+    # dv_j = sum_i p_ij do_i ; dk_j = sum_i sc q_i p_ij (do_i (v_j - o_i))
+    dv = [0.0, 0.0]
+    dk = [0.0, 0.0]
+    for i in range(2):
+        s = [sc * qv[i] * kv[0], sc * qv[i] * kv[1]]
+        p = [1.0 / (1.0 + math.exp(s[1] - s[0]))]
+        p.append(1.0 - p[0])
+        o = p[0] * vv[0] + p[1] * vv[1]
+        for j in range(2):
+            dv[j] += p[j] * dov[i]
+            dk[j] += sc * qv[i] * p[j] * dov[i] * (vv[j] - o)
+    for j in range(2):
+        ok &= abs(r["dv"][j, 0, 0] - dv[j]) < 1e-14
+        ok &= abs(r["dk"][j, 0, 0] - dk[j]) < 1e-14
+    return bool(ok)
+
+
+# ---------------------------------------------------------------- invariants
+
+def check_invariants(mod):
+    """P6 sum dk = 0; P7 sum dv = sum dout; P8 <Q,dQ> = <K,dK>, per clip and head."""
+    lens = [5, 17, 1, 30]
+    cu, q, k, v, do = rand_pack(lens, 3, 8, 4)
+    r = mod.attention(q, k, v, do, cu, 0.35)
+    ok = True
+    for s in range(len(lens)):
+        a, b = cu[s], cu[s + 1]
+        for h in range(3):
+            dk, dv, dq = r["dk"][a:b, h], r["dv"][a:b, h], r["dq"][a:b, h]
+            ok &= np.max(np.abs(dk.sum(0))) < 1e-12
+            ok &= np.allclose(dv.sum(0), do[a:b, h].sum(0), atol=1e-12)
+            ok &= abs(np.sum(q[a:b, h] * dq) - np.sum(k[a:b, h] * dk)) < 1e-11
+    return bool(ok)
+
+
+def check_delta_identity(mod):
+    """P9: Delta_i = sum_j P_ij dP_ij, with P and dP from plain loops."""
+    L, D, sc = 6, 4, 0.6
+    cu, q, k, v, do = rand_pack([L], 1, D, 5)
+    r = mod.attention(q, k, v, do, cu, sc)
+    ok = True
+    for i in range(L):
+        s = [sc * sum(q[i, 0, d] * k[j, 0, d] for d in range(D)) for j in range(L)]
+        m = max(s)
+        e = [math.exp(x - m) for x in s]
+        z = sum(e)
+        tot = sum(e[j] / z * sum(do[i, 0, d] * v[j, 0, d] for d in range(D)) for j in range(L))
+        ok &= abs(r["delta"][0, i] - tot) < 1e-13
+    return bool(ok)
+
+
+def check_key_shift(mod):
+    """P10: adding c to every key leaves out unchanged and adds scale*q.c to lse."""
+    cu, q, k, v, do = rand_pack([7, 12], 2, 8, 6)
+    c = np.random.default_rng(60).standard_normal(8)
+    sc = 0.4
+    r0 = mod.attention(q, k, v, do, cu, sc)
+    r1 = mod.attention(q, k + c, v, do, cu, sc)
+    ok = np.allclose(r0["out"], r1["out"], atol=1e-12)
+    ok &= np.allclose(r1["lse"] - r0["lse"], sc * np.einsum("thd,d->ht", q, c), atol=1e-12)
+    return bool(ok)
+
+
+def check_permutation_isolation(mod):
+    """P11: permuting clips permutes every output; editing one clip leaves the others."""
+    lens = [4, 9, 2, 13]
+    cu, q, k, v, do = rand_pack(lens, 2, 4, 7)
+    sc = 0.5
+    r = mod.attention(q, k, v, do, cu, sc)
+    perm = [2, 0, 3, 1]
+    idx = np.concatenate([np.arange(cu[s], cu[s + 1]) for s in perm])
+    cu2 = cu_from_lengths([lens[s] for s in perm])
+    r2 = mod.attention(q[idx], k[idx], v[idx], do[idx], cu2, sc)
+    ok = True
+    for key in ("out", "dq", "dk", "dv"):
+        ok &= np.allclose(r2[key], r[key][idx], atol=1e-13)
+    for key in ("lse", "delta"):
+        ok &= np.allclose(r2[key], r[key][:, idx], atol=1e-13)
+    q3 = q.copy()
+    q3[cu[1]:cu[2]] += 1.0  # edit clip 1 only
+    r3 = mod.attention(q3, k, v, do, cu, sc)
+    others = np.r_[cu[0]:cu[1], cu[2]:cu[4]]
+    for key in ("out", "dq", "dk", "dv"):
+        ok &= np.array_equal(r3[key][others], r[key][others])
+    return bool(ok)
+
+
+# ---------------------------------------------------------------- gradients
+
+def check_finite_differences(mod, lens=(1, 2, 3, 5, 17), H=2, D=4, seed=8):
+    """P12: dq, dk, dv equal central differences of <dout, out> (h = 1e-6)."""
+    cu, q, k, v, do = rand_pack(list(lens), H, D, seed)
+    sc = 0.45
+    r = mod.attention(q, k, v, do, cu, sc)
+
+    def f(qq, kk, vv):
+        return float(np.sum(do * mod.attention(qq, kk, vv, do, cu, sc)["out"]))
+
+    h = 1e-6
+    ok = True
+    for name, arr, pos in (("dq", q, 0), ("dk", k, 1), ("dv", v, 2)):
+        g = np.zeros_like(arr)
+        for ix in np.ndindex(arr.shape):
+            args_p = [q, k, v]
+            args_m = [q, k, v]
+            xp = arr.copy()
+            xm = arr.copy()
+            xp[ix] += h
+            xm[ix] -= h
+            args_p[pos] = xp
+            args_m[pos] = xm
+            g[ix] = (f(*args_p) - f(*args_m)) / (2 * h)
+        ok &= rel(r[name], g) < 1e-6
+    return bool(ok)
+
+
+def torch_reference(cu, q, k, v, do, sc):
+    """torch's SDPA (math path, float64, CPU) with a block-diagonal mask + autograd."""
+    import torch
+    T, H, D = q.shape
+    seg = np.zeros(T, dtype=np.int64)
+    for s in range(len(cu) - 1):
+        seg[cu[s]:cu[s + 1]] = s
+    segt = torch.from_numpy(seg)
+    mask = segt[:, None] == segt[None, :]
+    tq, tk, tv = (torch.tensor(np.ascontiguousarray(x.transpose(1, 0, 2))[None], dtype=torch.float64,
+                               requires_grad=True) for x in (q, k, v))
+    out = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, attn_mask=mask, scale=sc)
+    tdo = torch.tensor(np.ascontiguousarray(do.transpose(1, 0, 2))[None], dtype=torch.float64)
+    out.backward(tdo)
+    scores = sc * (tq.detach() @ tk.detach().transpose(-1, -2))
+    scores = scores.masked_fill(~mask, float("-inf"))
+    lse = torch.logsumexp(scores, dim=-1)[0]
+
+    def back(t):
+        return t[0].detach().numpy().transpose(1, 0, 2)
+
+    return {"out": back(out), "dq": back(tq.grad), "dk": back(tk.grad), "dv": back(tv.grad),
+            "lse": lse.numpy()}
+
+
+def check_torch_sdpa(mod):
+    """P15: agrees with torch's scaled_dot_product_attention + autograd to 1e-10."""
+    lens = [3, 1, 16, 7, 33]
+    cu, q, k, v, do = rand_pack(lens, 2, 8, 9)
+    sc = 1 / math.sqrt(8)
+    r = mod.attention(q, k, v, do, cu, sc)
+    t = torch_reference(cu, q, k, v, do, sc)
+    ok = True
+    for key in ("out", "dq", "dk", "dv", "lse"):
+        ok &= rel(r[key], t[key]) < 1e-10
+    return bool(ok)
+
+
+def brute_force(cu, q, k, v, do, sc):
+    """Pure-Python loops (no BLAS, math.exp) over the same definition."""
+    T, H, D = q.shape
+    res = {n: np.zeros((T, H, D)) for n in ("out", "dq", "dk", "dv")}
+    res["lse"] = np.zeros((H, T))
+    for s in range(len(cu) - 1):
+        a, b = int(cu[s]), int(cu[s + 1])
+        L = b - a
+        for h in range(H):
+            Q = [[float(q[a + i, h, d]) for d in range(D)] for i in range(L)]
+            K = [[float(k[a + i, h, d]) for d in range(D)] for i in range(L)]
+            V = [[float(v[a + i, h, d]) for d in range(D)] for i in range(L)]
+            G = [[float(do[a + i, h, d]) for d in range(D)] for i in range(L)]
+            P = []
+            for i in range(L):
+                srow = [sc * sum(Q[i][d] * K[j][d] for d in range(D)) for j in range(L)]
+                m = max(srow)
+                e = [math.exp(x - m) for x in srow]
+                z = math.fsum(e)
+                P.append([x / z for x in e])
+                res["lse"][h, a + i] = m + math.log(z)
+            O = [[math.fsum(P[i][j] * V[j][d] for j in range(L)) for d in range(D)] for i in range(L)]
+            for i in range(L):
+                dl = math.fsum(G[i][d] * O[i][d] for d in range(D))
+                for j in range(L):
+                    dp = math.fsum(G[i][d] * V[j][d] for d in range(D))
+                    ds = P[i][j] * (dp - dl)
+                    for d in range(D):
+                        res["dq"][a + i, h, d] += sc * ds * K[j][d]
+                        res["dk"][a + j, h, d] += sc * ds * Q[i][d]
+                        res["dv"][a + j, h, d] += P[i][j] * G[i][d]
+                for d in range(D):
+                    res["out"][a + i, h, d] = O[i][d]
+    return res
+
+
+def check_brute_force(mod):
+    """P13: the blocked BLAS oracle equals plain loops to 1e-12."""
+    lens = [1, 2, 3, 5, 17]
+    cu, q, k, v, do = rand_pack(lens, 2, 4, 10)
+    r = mod.attention(q, k, v, do, cu, 0.55)
+    b = brute_force(cu, q, k, v, do, 0.55)
+    return all(rel(r[key], b[key]) < 1e-12 for key in ("out", "dq", "dk", "dv", "lse"))
+
+
+PINS = {
+    "P1_len1": check_len1,
+    "P2_equal_v": check_equal_v,
+    "P3_equal_k": check_equal_k,
+    "P4_len2_by_hand": check_len2_by_hand,
+    "P6_P7_P8_invariants": check_invariants,
+    "P9_delta": check_delta_identity,
+    "P10_key_shift": check_key_shift,
+    "P11_permutation_isolation": check_permutation_isolation,
+    "P12_finite_differences": check_finite_differences,
+    "P13_brute_force": check_brute_force,
+    "P15_torch_sdpa": check_torch_sdpa,
+}
+
+
+@pytest.mark.parametrize("name", sorted(PINS))
+def test_pin(name):
+    assert PINS[name](orc), name
+
+
+def test_rows_sum_to_one():
+    """P5: the oracle's own row check (|sum_j P_ij - 1| <= 1e-12) holds."""
+    cu, q, k, v, do = rand_pack([40, 3, 100], 2, 16, 11)
+    orc.attention(q, k, v, do, cu, 1.7, check_rows=True)
+
+
+@pytest.mark.parametrize("block", [1, 7, 100, 512])
+def test_block_size_independence(block):
+    """P14: the row-block size changes nothing beyond rounding."""
+    cu, q, k, v, do = rand_pack([100, 37], 2, 8, 12)
+    ref = orc.attention(q, k, v, do, cu, 0.3, block_rows=100)
+    r = orc.attention(q, k, v, do, cu, 0.3, block_rows=block)
+    for key in ("out", "dq", "dk", "dv", "lse", "delta"):
+        assert rel(r[key], ref[key]) < 1e-12, key
+
+
+def test_heads_independent():
+    """P11 (heads): computing a head subset gives the same values for those heads."""
+    cu, q, k, v, do = rand_pack([20, 9], 4, 8, 13)
+    full = orc.attention(q, k, v, do, cu, 0.4)
+    sub = orc.attention(q, k, v, do, cu, 0.4, heads=[1, 3])
+    for key in ("out", "dq", "dk", "dv"):
+        assert np.array_equal(sub[key][:, [1, 3]], full[key][:, [1, 3]])
+        assert np.all(sub[key][:, [0, 2]] == 0)
+
+
+def test_zero_length_clips_skipped():
+    """Empty clips contribute nothing and disturb nothing."""
+    cu, q, k, v, do = rand_pack([5, 0, 6, 0], 2, 4, 14)
+    r = orc.attention(q, k, v, do, cu, 0.5)
+    cu2 = cu_from_lengths([5, 6])
+    r2 = orc.attention(q, k, v, do, cu2, 0.5)
+    for key in ("out", "dq", "dk", "dv", "lse"):
+        assert np.array_equal(r[key], r2[key])
+
+
+def test_query_rows_match_full():
+    """Row-sampled out/lse/dq equal the full oracle at those rows."""
+    lens = [50, 1, 70]
+    cu, q, k, v, do = rand_pack(lens, 3, 8, 15)
+    full = orc.attention(q, k, v, do, cu, 0.3)
+    toks = [0, 49, 50, 51, 120, 77]
+    hs = [0, 2, 1, 0, 2, 1]
+    r = orc.query_rows(q, k, v, do, cu, 0.3, toks, hs)
+    for i, (t, h) in enumerate(zip(toks, hs)):
+        assert np.allclose(r["out"][i], full["out"][t, h], atol=1e-13)
+        assert abs(r["lse"][i] - full["lse"][h, t]) < 1e-13
+        assert np.allclose(r["dq"][i], full["dq"][t, h], atol=1e-13)
+
+
+def test_key_rows_match_full():
+    """Key-sampled dk/dv equal the full oracle at those keys."""
+    lens = [30, 90]
+    cu, q, k, v, do = rand_pack(lens, 2, 8, 16)
+    full = orc.attention(q, k, v, do, cu, 0.3)
+    keys = [0, 5, 89]
+    r = orc.key_rows(q, k, v, do, cu, 0.3, seq=1, head=1, keys=keys, block_rows=17)
+    for i, j in enumerate(keys):
+        assert np.allclose(r["dk"][i], full["dk"][30 + j, 1], atol=1e-13)
+        assert np.allclose(r["dv"][i], full["dv"][30 + j, 1], atol=1e-13)
+
+
+def test_bf16_inputs_are_exact():
+    """The oracle sees the generator's bf16 values exactly (float32 widening is lossless)."""
+    p = make_pack([33, 5], 2, 8, seed=3)
+    q = p.f32("q")
+    assert q.dtype == np.float32
+    assert np.array_equal(q.astype(np.float64).astype(np.float32), q)
+    # bf16 values have only 8 significant bits: the low 16 bits of float32 are zero
+    assert np.all((q.view(np.uint32) & 0xFFFF) == 0)
+
+
+# ---------------------------------------------------------------- planted mistakes
+
+MUTANTS = {
+    "softmax_unnormalised": ("return E / l[:, None], m, l", "return E, m, l"),
+    "dS_sign": ("P * (dP - delta[:, None])", "P * (dP + delta[:, None])"),
+    "dK_no_scale": ("dK += scale * (dS.T @ Qb)", "dK += (dS.T @ Qb)"),
+    "dV_transposed": ("dV += P.T @ dOb", "dV += P @ dOb"),
+    "lse_log2": ("lse[r0:r1] = m + np.log(l)", "lse[r0:r1] = m + np.log2(l)"),
+    "lse_no_max": ("lse[r0:r1] = m + np.log(l)", "lse[r0:r1] = np.log(l)"),
+    "delta_from_v": ("db = np.sum(dOb * Ob, axis=1)", "db = np.sum(dOb * V[r0:r1], axis=1)"),
+    "scores_no_scale": ("return scale * (Qb @ K.T)", "return (Qb @ K.T)"),
+    "dQ_uses_V": ("dQ[r0:r1] = scale * (dS @ K)", "dQ[r0:r1] = scale * (dS @ V)"),
+    "dK_uses_K": ("dK += scale * (dS.T @ Qb)", "dK += scale * (dS.T @ K[r0:r1])"),
+    "dP_uses_K": ("dP = dOb @ V.T", "dP = dOb @ K.T"),
+}
+
+
+def mutant_module(old, new):
+    src = open(orc.__file__).read()
+    assert src.count(old) >= 1, f"mutation site not found: {old}"
+    mod = types.ModuleType("oracle_mutant")
+    exec(compile(src.replace(old, new), "oracle_mutant", "exec"), mod.__dict__)
+    return mod
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutants_are_caught(name):
+    mod = mutant_module(*MUTANTS[name])
+    failing = []
+    for pin, fn in PINS.items():
+        if pin in ("P12_finite_differences", "P13_brute_force"):
+            continue  # the cheaper pins must already catch every mutant
+        try:
+            if not fn(mod):
+                failing.append(pin)
+        except Exception:  # a shape error is also a detection
+            failing.append(pin)
+    assert failing, f"mutant {name} passed every pin"
