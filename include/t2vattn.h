@@ -1,0 +1,122 @@
+/*
+ * libt2vattn: bidirectional multi-head self-attention, forward and backward,
+ * over packed variable-length token sequences, for AMD MI355X (gfx950).
+ *
+ * The operation (paper Section III, Observation 2): every clip is one sequence
+ * of 3D latent patches, and each token attends to every token of its own clip
+ * (full, non-causal self-attention), at O(L^2) cost per clip -- the alpha_2 *
+ * B * S^2 term of the DiT latency model, Eq. (9). Clips are packed back to back
+ * along the token axis and described by cu_seqlens, so clips of different
+ * resolution and duration share one call without padding (Section II-B
+ * contrasts padding, packing and bucketing). The training step runs this
+ * operation forward and backward (Fig. 1 caption: DiT backward pass).
+ *
+ * For clip s (tokens cu[s] .. cu[s+1]-1, length L = cu[s+1]-cu[s]) and head h,
+ * with Q, K, V, dO the [L, D] slices:
+ *   S = scale * Q K^T;  P = softmax over each row of S;  out = P V;
+ *   lse_i = ln(sum_j exp(S_ij))   (natural log, the row normaliser);
+ *   Delta_i = sum_d dO_id out_id;  dP = dO V^T;  dS = P * (dP - Delta);
+ *   dq = scale * dS K;  dk = scale * dS^T Q;  dv = P^T dO.
+ * Gradients are those of the scalar <dout, out>; lse is not differentiated.
+ *
+ * Layout. Every tensor is row-major and contiguous, "THD": element (t, h, d)
+ * of a [T, H, D] tensor sits at ((t * H) + h) * D + d. q, k, v, out, dout, dq,
+ * dk, dv are bfloat16 (passed as void*). lse and delta_ws are float32 laid
+ * out [H, T]: element (h, t) at h * T + t. T = cu_seqlens[nseq].
+ *
+ * Ownership. The caller owns every buffer. Tensor pointers are device
+ * pointers; cu_seqlens is a HOST pointer (the tile scheduler runs on the
+ * host). The library keeps only a cache of device work lists keyed by the
+ * contents of cu_seqlens (released by t2v_release_cache).
+ *
+ * Errors. Every function returns a t2v_status. Arguments are validated before
+ * anything is launched, so a rejected call writes nothing. Execution is
+ * asynchronous on `stream` (a hipStream_t; NULL is the default stream). A
+ * kernel launch failure returns T2V_ERR_HIP. t2v_last_error() describes the
+ * last non-OK status of the calling thread. No C++ exception crosses the ABI.
+ * T = 0 returns T2V_OK without launching anything; zero-length clips are
+ * skipped. Calls on different streams may run concurrently.
+ */
+#ifndef T2VATTN_H
+#define T2VATTN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  T2V_OK = 0,
+  T2V_ERR_INVALID_ARG = 1, /* bad pointer, size, cu_seqlens, scale or aliasing */
+  T2V_ERR_UNSUPPORTED = 2, /* head_dim other than 64 or 128 */
+  T2V_ERR_HIP = 3,         /* a HIP runtime call or kernel launch failed */
+  T2V_ERR_OOM = 4          /* the work-list cache could not allocate */
+} t2v_status;
+
+/* Tile orders for the scheduler (see t2v_build_worklist). */
+typedef enum {
+  T2V_ORDER_NATURAL = 0,      /* clip, head, tile in pack order */
+  T2V_ORDER_LONGEST_FIRST = 1 /* clips by length descending; (clip, head) tiles kept adjacent;
+                                 dealt to the 8 XCDs in cost-balanced contiguous runs */
+} t2v_order;
+
+/* Forward pass: out = softmax(scale * q k^T) v per clip and head, and lse.
+ *   q, k, v    device bf16 [T, H, D], 16-byte aligned, read only
+ *   cu_seqlens host int32 [nseq + 1]: cu[0] = 0, non-decreasing, cu[nseq] = T < 2^31
+ *   nseq       number of clips (>= 0); heads = H (>= 1); head_dim = D in {64, 128}
+ *   scale      finite multiplier of q k^T (1/sqrt(D) in the usual case)
+ *   out        device bf16 [T, H, D], written; must not overlap any input
+ *   lse        device fp32 [H, T], written; natural-log row normaliser
+ *   stream     hipStream_t to launch on
+ */
+int t2v_attn_fwd(const void* q, const void* k, const void* v,
+                 const int32_t* cu_seqlens, int nseq, int heads, int head_dim, float scale,
+                 void* out, float* lse, void* stream);
+
+/* Backward pass for the loss <dout, out>: dq, dk, dv.
+ *   q, k, v, cu_seqlens, nseq, heads, head_dim, scale   as passed to t2v_attn_fwd
+ *   out, lse   the forward outputs for the same inputs (device, read only)
+ *   dout       device bf16 [T, H, D], the gradient of the loss w.r.t. out
+ *   dq, dk, dv device bf16 [T, H, D], written; must not overlap each other or any input
+ *   delta_ws   device fp32 [H, T], caller-owned scratch; receives Delta = rowsum(dout * out)
+ *   stream     hipStream_t to launch on
+ * Deterministic: no atomics; repeated calls give bitwise-equal results.
+ */
+int t2v_attn_bwd(const void* q, const void* k, const void* v,
+                 const void* out, const float* lse,
+                 const int32_t* cu_seqlens, int nseq, int heads, int head_dim, float scale,
+                 const void* dout, void* dq, void* dk, void* dv, float* delta_ws,
+                 void* stream);
+
+/* Thread-local message describing the last non-OK status of this thread. */
+const char* t2v_last_error(void);
+
+/* Waits for the device, then frees every cached work list. Safe to call at any time. */
+void t2v_release_cache(void);
+
+/* Host-only scheduler, exposed for testing. Builds the work list the kernels use for
+ * tiles of `block` rows: each item is 4 int32 {row0 of the clip, clip length L,
+ * first row of the tile within the clip, head}. Clips of length 0 give no items.
+ *   order       a t2v_order
+ *   items_out   host int32 [capacity * 4], or NULL to query the count only
+ *   n_items_out receives the number of items
+ * Returns T2V_ERR_INVALID_ARG if capacity is too small (n_items_out is still set).
+ */
+int t2v_build_worklist(const int32_t* cu_seqlens, int nseq, int heads, int block, int order,
+                       int32_t* items_out, int capacity, int* n_items_out);
+
+/* Host-only: the predicted makespan of a work list on `slots` identical workers, in units
+ * of (rows x keys) tile cost, when items are taken in list order by the next free worker
+ * (greedy list scheduling), plus the lower bound max(total / slots, largest item). */
+int t2v_plan_makespan(const int32_t* items, int n_items, int block, int slots,
+                      double* makespan_out, double* lower_bound_out);
+
+/* Library version, for diagnostics. */
+const char* t2v_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* T2VATTN_H */

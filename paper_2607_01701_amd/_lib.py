@@ -1,0 +1,208 @@
+"""ctypes binding to libt2vattn: argument marshalling only.
+
+Every step of the computation runs in the HIP library; this module only turns
+torch tensors and numpy arrays into pointers and sizes, and raises on a non-OK
+status. There is no fallback: if the library is missing, calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libt2vattn.so")
+HOST_LIB_PATH = os.path.join(_PKG, "libt2vattn_host.so")
+
+T2V_OK = 0
+T2V_ERR_INVALID_ARG = 1
+T2V_ERR_UNSUPPORTED = 2
+T2V_ERR_HIP = 3
+T2V_ERR_OOM = 4
+STATUS_NAMES = {0: "T2V_OK", 1: "T2V_ERR_INVALID_ARG", 2: "T2V_ERR_UNSUPPORTED", 3: "T2V_ERR_HIP",
+                4: "T2V_ERR_OOM"}
+
+ORDER_NATURAL = 0
+ORDER_LONGEST_FIRST = 1
+
+# Symbols declared in include/t2vattn.h.
+EXPORTS = ("t2v_attn_fwd", "t2v_attn_bwd", "t2v_last_error", "t2v_release_cache", "t2v_build_worklist",
+           "t2v_plan_makespan", "t2v_version")
+HOST_EXPORTS = ("t2v_last_error", "t2v_build_worklist", "t2v_plan_makespan", "t2v_version")
+
+_vp = ctypes.c_void_p
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_f32p = ctypes.c_void_p  # device float* passed as an address
+
+
+class T2VError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+def _declare(lib, full: bool):
+    lib.t2v_last_error.restype = ctypes.c_char_p
+    lib.t2v_last_error.argtypes = []
+    lib.t2v_version.restype = ctypes.c_char_p
+    lib.t2v_version.argtypes = []
+    lib.t2v_build_worklist.restype = ctypes.c_int
+    lib.t2v_build_worklist.argtypes = [_i32p, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, _i32p,
+                                       ctypes.c_int, ctypes.POINTER(ctypes.c_int)]
+    lib.t2v_plan_makespan.restype = ctypes.c_int
+    lib.t2v_plan_makespan.argtypes = [_i32p, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                      ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
+    if full:
+        lib.t2v_attn_fwd.restype = ctypes.c_int
+        lib.t2v_attn_fwd.argtypes = [_vp, _vp, _vp, _i32p, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                     ctypes.c_float, _vp, _f32p, _vp]
+        lib.t2v_attn_bwd.restype = ctypes.c_int
+        lib.t2v_attn_bwd.argtypes = [_vp, _vp, _vp, _vp, _f32p, _i32p, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                     ctypes.c_float, _vp, _vp, _vp, _vp, _f32p, _vp]
+        lib.t2v_release_cache.restype = None
+        lib.t2v_release_cache.argtypes = []
+    return lib
+
+
+_lib = None
+_host_lib = None
+
+
+def lib():
+    """The HIP library (loaded once). Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2607_01701_amd.build`")
+        _lib = _declare(ctypes.CDLL(LIB_PATH), full=True)
+    return _lib
+
+
+def host_lib():
+    """The host-only scheduler library (g++ build, no HIP)."""
+    global _host_lib
+    if _host_lib is None:
+        if not os.path.exists(HOST_LIB_PATH):
+            raise ImportError(f"{HOST_LIB_PATH} is missing: build it with `python -m paper_2607_01701_amd.build`")
+        _host_lib = _declare(ctypes.CDLL(HOST_LIB_PATH), full=False)
+    return _host_lib
+
+
+def _cu_array(cu_seqlens) -> np.ndarray:
+    a = np.ascontiguousarray(np.asarray(cu_seqlens, dtype=np.int32))
+    if a.ndim != 1 or a.shape[0] < 1:
+        raise ValueError("cu_seqlens must be a 1-D array with nseq + 1 entries")
+    return a
+
+
+def _check(L, status: int):
+    if status != T2V_OK:
+        raise T2VError(status, L.t2v_last_error().decode())
+
+
+# ----------------------------------------------------------------- raw C-ABI names
+
+def t2v_attn_fwd(q, k, v, cu_seqlens, nseq, heads, head_dim, scale, out, lse, stream):
+    """Direct call of t2v_attn_fwd with integer addresses; returns the status."""
+    cu = _cu_array(cu_seqlens)
+    return lib().t2v_attn_fwd(q, k, v, cu.ctypes.data_as(_i32p), nseq, heads, head_dim, scale, out, lse, stream)
+
+
+def t2v_attn_bwd(q, k, v, out, lse, cu_seqlens, nseq, heads, head_dim, scale, dout, dq, dk, dv, delta_ws,
+                 stream):
+    """Direct call of t2v_attn_bwd with integer addresses; returns the status."""
+    cu = _cu_array(cu_seqlens)
+    return lib().t2v_attn_bwd(q, k, v, out, lse, cu.ctypes.data_as(_i32p), nseq, heads, head_dim, scale, dout,
+                              dq, dk, dv, delta_ws, stream)
+
+
+def t2v_last_error(L=None) -> str:
+    return (L or lib()).t2v_last_error().decode()
+
+
+def t2v_release_cache() -> None:
+    lib().t2v_release_cache()
+
+
+def t2v_version(L=None) -> str:
+    return (L or lib()).t2v_version().decode()
+
+
+def t2v_build_worklist(cu_seqlens, heads: int, block: int, order: int = ORDER_LONGEST_FIRST, L=None) -> np.ndarray:
+    """The scheduler's work list as an int32 array [n_items, 4] = (row0, len, tile0, head)."""
+    L = L or host_lib()
+    cu = _cu_array(cu_seqlens)
+    nseq = cu.shape[0] - 1
+    n = ctypes.c_int(0)
+    _check(L, L.t2v_build_worklist(cu.ctypes.data_as(_i32p), nseq, heads, block, order, None, 0, ctypes.byref(n)))
+    items = np.zeros((n.value, 4), dtype=np.int32)
+    _check(L, L.t2v_build_worklist(cu.ctypes.data_as(_i32p), nseq, heads, block, order,
+                                   items.ctypes.data_as(_i32p), n.value, ctypes.byref(n)))
+    return items
+
+
+def t2v_plan_makespan(items: np.ndarray, block: int, slots: int, L=None):
+    """(greedy list-scheduling makespan, lower bound) of a work list, in rows x keys."""
+    L = L or host_lib()
+    it = np.ascontiguousarray(items, dtype=np.int32)
+    ms, lb = ctypes.c_double(0), ctypes.c_double(0)
+    _check(L, L.t2v_plan_makespan(it.ctypes.data_as(_i32p), it.shape[0], block, slots, ctypes.byref(ms),
+                                  ctypes.byref(lb)))
+    return ms.value, lb.value
+
+
+# ----------------------------------------------------------------- torch convenience
+
+def _stream_handle(stream):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _check_tensor(t, name, T, H, D):
+    import torch
+    if not t.is_cuda or t.dtype != torch.bfloat16 or not t.is_contiguous() or tuple(t.shape) != (T, H, D):
+        raise ValueError(f"{name} must be a contiguous CUDA bfloat16 tensor of shape {(T, H, D)}")
+
+
+def attn_fwd(q, k, v, cu_seqlens, scale: float, out=None, lse=None, stream=None):
+    """Forward pass on torch tensors q, k, v [T, H, D] (bf16, on the GPU).
+
+    Returns (out [T, H, D] bf16, lse [H, T] fp32).
+    """
+    import torch
+    T, H, D = q.shape
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _check_tensor(t, name, T, H, D)
+    cu = _cu_array(cu_seqlens)
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((H, T), dtype=torch.float32, device=q.device)
+    L = lib()
+    st = L.t2v_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), cu.ctypes.data_as(_i32p), cu.shape[0] - 1, H, D,
+                        float(scale), out.data_ptr(), lse.data_ptr(), _stream_handle(stream))
+    _check(L, st)
+    return out, lse
+
+
+def attn_bwd(q, k, v, out, lse, dout, cu_seqlens, scale: float, dq=None, dk=None, dv=None, delta_ws=None,
+             stream=None):
+    """Backward pass; returns (dq, dk, dv) bf16 [T, H, D]."""
+    import torch
+    T, H, D = q.shape
+    for name, t in (("q", q), ("k", k), ("v", v), ("out", out), ("dout", dout)):
+        _check_tensor(t, name, T, H, D)
+    cu = _cu_array(cu_seqlens)
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(q) if dk is None else dk
+    dv = torch.empty_like(q) if dv is None else dv
+    if delta_ws is None:
+        delta_ws = torch.empty((H, T), dtype=torch.float32, device=q.device)
+    L = lib()
+    st = L.t2v_attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
+                        cu.ctypes.data_as(_i32p), cu.shape[0] - 1, H, D, float(scale), dout.data_ptr(),
+                        dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), delta_ws.data_ptr(), _stream_handle(stream))
+    _check(L, st)
+    return dq, dk, dv

@@ -1,0 +1,248 @@
+// C ABI of libt2vattn: argument validation, the device work-list cache, and launches.
+#include <hip/hip_runtime.h>
+
+#include <cstdlib>
+#include <cstring>
+#include <list>
+#include <memory>
+#include <mutex>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/t2vattn.h"
+#include "t2v_host.h"
+#include "t2v_kernels.h"
+
+namespace t2v {
+namespace {
+
+int hip_fail(hipError_t e, const char* what) {
+  return set_error(T2V_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+// The scheduler order: longest clip first unless T2V_ORDER=natural (for ablations).
+int order_from_env() {
+  const char* s = std::getenv("T2V_ORDER");
+  if (s != nullptr && std::strcmp(s, "natural") == 0) return T2V_ORDER_NATURAL;
+  return T2V_ORDER_LONGEST_FIRST;
+}
+
+// cu_seqlens must be host memory: the scheduler reads it on the host.
+int check_host_pointer(const int32_t* cu) {
+  hipPointerAttribute_t attr;
+  std::memset(&attr, 0, sizeof(attr));
+  const hipError_t e = hipPointerGetAttributes(&attr, cu);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();  // plain pageable host memory is not known to HIP
+    return T2V_OK;
+  }
+  if (attr.type == hipMemoryTypeDevice)
+    return set_error(T2V_ERR_INVALID_ARG, "cu_seqlens must be a host pointer, got device memory");
+  return T2V_OK;
+}
+
+// Immutable device copies of work lists, keyed by everything that shapes them.
+struct Plan {
+  std::vector<int32_t> cu;
+  int heads = 0, block = 0, order = 0, device = 0;
+  Item* d_items = nullptr;
+  Item* h_items = nullptr;  // pinned source of the upload, kept for the entry's life
+  int n_items = 0;
+  hipEvent_t ready = nullptr;     // upload finished
+  hipEvent_t last_use = nullptr;  // last launch that read d_items
+  ~Plan() {
+    if (last_use != nullptr) (void)hipEventSynchronize(last_use);
+    if (ready != nullptr) (void)hipEventSynchronize(ready);
+    if (d_items != nullptr) (void)hipFree(d_items);
+    if (h_items != nullptr) (void)hipHostFree(h_items);
+    if (ready != nullptr) (void)hipEventDestroy(ready);
+    if (last_use != nullptr) (void)hipEventDestroy(last_use);
+  }
+};
+
+constexpr size_t kMaxPlans = 64;
+
+class PlanCache {
+ public:
+  // Returns the plan (creating and uploading it on `stream` if new) with the
+  // upload ordered before any later work on `stream`.
+  int get(const int32_t* cu, int nseq, int heads, int block, int order, hipStream_t stream, Plan** out) {
+    int device = 0;
+    hipError_t e = hipGetDevice(&device);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    std::lock_guard<std::mutex> lock(mu_);
+    for (auto itr = plans_.begin(); itr != plans_.end(); ++itr) {
+      Plan& p = **itr;
+      if (p.heads == heads && p.block == block && p.order == order && p.device == device &&
+          p.cu.size() == static_cast<size_t>(nseq + 1) &&
+          std::memcmp(p.cu.data(), cu, sizeof(int32_t) * (nseq + 1)) == 0) {
+        plans_.splice(plans_.begin(), plans_, itr);  // most recently used first
+        e = hipStreamWaitEvent(stream, p.ready, 0);
+        if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
+        *out = &p;
+        return T2V_OK;
+      }
+    }
+    std::unique_ptr<Plan> p(new Plan());
+    p->cu.assign(cu, cu + nseq + 1);
+    p->heads = heads;
+    p->block = block;
+    p->order = order;
+    p->device = device;
+    std::vector<Item> items = build_worklist(cu, nseq, heads, block, order);
+    p->n_items = static_cast<int>(items.size());
+    const size_t bytes = items.size() * sizeof(Item);
+    if (bytes > 0) {
+      e = hipMalloc(&p->d_items, bytes);
+      if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return set_error(T2V_ERR_OOM, "hipMalloc of the work list failed");
+      }
+      e = hipHostMalloc(&p->h_items, bytes, hipHostMallocDefault);
+      if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return set_error(T2V_ERR_OOM, "hipHostMalloc of the work-list staging failed");
+      }
+      std::memcpy(p->h_items, items.data(), bytes);
+    }
+    e = hipEventCreateWithFlags(&p->ready, hipEventDisableTiming);
+    if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
+    e = hipEventCreateWithFlags(&p->last_use, hipEventDisableTiming);
+    if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
+    if (bytes > 0) {
+      e = hipMemcpyAsync(p->d_items, p->h_items, bytes, hipMemcpyHostToDevice, stream);
+      if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync of the work list");
+    }
+    e = hipEventRecord(p->ready, stream);
+    if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+    plans_.push_front(std::move(p));
+    while (plans_.size() > kMaxPlans) plans_.pop_back();  // waits for the evicted plan's last use
+    *out = plans_.front().get();
+    return T2V_OK;
+  }
+
+  int mark_used(Plan* p, hipStream_t stream) {
+    std::lock_guard<std::mutex> lock(mu_);
+    const hipError_t e = hipEventRecord(p->last_use, stream);
+    if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+    return T2V_OK;
+  }
+
+  void clear() {
+    std::lock_guard<std::mutex> lock(mu_);
+    plans_.clear();
+  }
+
+ private:
+  std::mutex mu_;
+  std::list<std::unique_ptr<Plan>> plans_;
+};
+
+PlanCache& cache() {
+  static PlanCache* c = new PlanCache();  // never destroyed: no HIP calls at process exit
+  return *c;
+}
+
+int64_t tensor_bytes(int64_t T, int heads, int head_dim) { return T * heads * head_dim * 2; }
+
+}  // namespace
+}  // namespace t2v
+
+extern "C" {
+
+int t2v_attn_fwd(const void* q, const void* k, const void* v, const int32_t* cu_seqlens, int nseq, int heads,
+                 int head_dim, float scale, void* out, float* lse, void* stream) {
+  using namespace t2v;
+  try {
+    int64_t T = 0;
+    if (int st = validate_shape(cu_seqlens, nseq, heads, head_dim, scale, &T)) return st;
+    if (T == 0) return T2V_OK;
+    const int64_t tb = tensor_bytes(T, heads, head_dim);
+    const int64_t lb = T * heads * 4;
+    if (int st = validate_pointers({{q, tb, "q"}, {k, tb, "k"}, {v, tb, "v"}}, {{out, tb, "out"}, {lse, lb, "lse"}}))
+      return st;
+    if (int st = check_host_pointer(cu_seqlens)) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    Plan* plan = nullptr;
+    if (int st = cache().get(cu_seqlens, nseq, heads, fwd_tile_rows(head_dim), order_from_env(), s, &plan)) return st;
+    if (plan->n_items == 0) return T2V_OK;
+    AttnArgs a{};
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.heads = heads;
+    a.head_dim = head_dim;
+    a.total_tokens = T;
+    a.scale = scale;
+    hipError_t e = launch_fwd(a, out, lse, plan->d_items, plan->n_items, s);
+    if (e != hipSuccess) return hip_fail(e, "forward kernel launch");
+    return cache().mark_used(plan, s);
+  } catch (const std::bad_alloc&) {
+    return set_error(T2V_ERR_OOM, "host allocation failed");
+  } catch (...) {
+    return set_error(T2V_ERR_INVALID_ARG, "unexpected host exception");
+  }
+}
+
+int t2v_attn_bwd(const void* q, const void* k, const void* v, const void* out, const float* lse,
+                 const int32_t* cu_seqlens, int nseq, int heads, int head_dim, float scale, const void* dout,
+                 void* dq, void* dk, void* dv, float* delta_ws, void* stream) {
+  using namespace t2v;
+  try {
+    int64_t T = 0;
+    if (int st = validate_shape(cu_seqlens, nseq, heads, head_dim, scale, &T)) return st;
+    if (T == 0) return T2V_OK;
+    const int64_t tb = tensor_bytes(T, heads, head_dim);
+    const int64_t lb = T * heads * 4;
+    if (int st = validate_pointers(
+            {{q, tb, "q"}, {k, tb, "k"}, {v, tb, "v"}, {out, tb, "out"}, {lse, lb, "lse"}, {dout, tb, "dout"}},
+            {{dq, tb, "dq"}, {dk, tb, "dk"}, {dv, tb, "dv"}, {delta_ws, lb, "delta_ws"}}))
+      return st;
+    if (int st = check_host_pointer(cu_seqlens)) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int order = order_from_env();
+    Plan* pk = nullptr;
+    Plan* pq = nullptr;
+    if (int st = cache().get(cu_seqlens, nseq, heads, dkdv_tile_rows(head_dim), order, s, &pk)) return st;
+    if (int st = cache().get(cu_seqlens, nseq, heads, dq_tile_rows(head_dim), order, s, &pq)) return st;
+    AttnArgs a{};
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.out = out;
+    a.lse = lse;
+    a.dout = dout;
+    a.dq = dq;
+    a.dk = dk;
+    a.dv = dv;
+    a.delta = delta_ws;
+    a.heads = heads;
+    a.head_dim = head_dim;
+    a.total_tokens = T;
+    a.scale = scale;
+    hipError_t e = launch_bwd_pre(a, s);
+    if (e != hipSuccess) return hip_fail(e, "backward preprocess launch");
+    if (pk->n_items > 0) {
+      e = launch_bwd_dkdv(a, pk->d_items, pk->n_items, s);
+      if (e != hipSuccess) return hip_fail(e, "dK/dV kernel launch");
+    }
+    if (pq->n_items > 0) {
+      e = launch_bwd_dq(a, pq->d_items, pq->n_items, s);
+      if (e != hipSuccess) return hip_fail(e, "dQ kernel launch");
+    }
+    if (int st = cache().mark_used(pk, s)) return st;
+    return cache().mark_used(pq, s);
+  } catch (const std::bad_alloc&) {
+    return set_error(T2V_ERR_OOM, "host allocation failed");
+  } catch (...) {
+    return set_error(T2V_ERR_INVALID_ARG, "unexpected host exception");
+  }
+}
+
+void t2v_release_cache(void) {
+  (void)hipDeviceSynchronize();
+  t2v::cache().clear();
+}
+
+}  // extern "C"

@@ -1,0 +1,219 @@
+// Host-side validation and tile scheduling for libt2vattn (no HIP dependency).
+//
+// The scheduler mirrors, inside one GPU, the balance goal of the paper's planner:
+// a clip's attention cost grows with L^2 (Eq. (9), alpha_2 * B * S^2), so a pack of
+// clips of very different length (Section III, Observation 1; the 13- to 113-frame
+// example of Fig. 1) leaves workers idle unless the longest work starts first. The
+// planner's fitness function is a critical-path list scheduler; here every tile of a
+// clip costs (tile rows x L) and the list is ordered longest clip first, which is
+// greedy list scheduling in LPT order for the hardware's in-order dispatch.
+#include "t2v_host.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <numeric>
+#include <queue>
+
+#include "../../include/t2vattn.h"
+
+namespace t2v {
+
+namespace {
+thread_local std::string g_last_error;
+}
+
+int set_error(int status, const std::string& msg) {
+  g_last_error = msg;
+  return status;
+}
+
+const char* last_error() { return g_last_error.c_str(); }
+
+int validate_shape(const int32_t* cu, int nseq, int heads, int head_dim, float scale, int64_t* total_tokens) {
+  if (nseq < 0) return set_error(T2V_ERR_INVALID_ARG, "nseq must be >= 0");
+  if (cu == nullptr) return set_error(T2V_ERR_INVALID_ARG, "cu_seqlens is NULL");
+  if (heads < 1) return set_error(T2V_ERR_INVALID_ARG, "heads must be >= 1");
+  if (head_dim != 64 && head_dim != 128)
+    return set_error(T2V_ERR_UNSUPPORTED, "head_dim must be 64 or 128, got " + std::to_string(head_dim));
+  if (!std::isfinite(scale)) return set_error(T2V_ERR_INVALID_ARG, "scale must be finite");
+  if (cu[0] != 0) return set_error(T2V_ERR_INVALID_ARG, "cu_seqlens[0] must be 0");
+  for (int s = 0; s < nseq; ++s) {
+    if (cu[s + 1] < cu[s])
+      return set_error(T2V_ERR_INVALID_ARG, "cu_seqlens must be non-decreasing (index " + std::to_string(s + 1) + ")");
+  }
+  const int64_t T = cu[nseq];
+  // Element offsets are 64-bit in the kernels; bound T*H*D so byte sizes fit comfortably.
+  const int64_t elems = T * static_cast<int64_t>(heads) * head_dim;
+  if (heads > (1 << 20) || elems > (int64_t(1) << 40))
+    return set_error(T2V_ERR_INVALID_ARG, "T * heads * head_dim is too large");
+  *total_tokens = T;
+  return T2V_OK;
+}
+
+int validate_pointers(const std::vector<Range>& inputs, const std::vector<Range>& outputs) {
+  auto check = [](const Range& r) -> int {
+    if (r.ptr == nullptr) return set_error(T2V_ERR_INVALID_ARG, std::string(r.name) + " is NULL");
+    if (reinterpret_cast<uintptr_t>(r.ptr) % 16 != 0)
+      return set_error(T2V_ERR_INVALID_ARG, std::string(r.name) + " is not 16-byte aligned");
+    return T2V_OK;
+  };
+  for (const auto& r : inputs)
+    if (int st = check(r)) return st;
+  for (const auto& r : outputs)
+    if (int st = check(r)) return st;
+  auto overlap = [](const Range& a, const Range& b) {
+    const auto a0 = reinterpret_cast<uintptr_t>(a.ptr), b0 = reinterpret_cast<uintptr_t>(b.ptr);
+    return a0 < b0 + static_cast<uintptr_t>(b.bytes) && b0 < a0 + static_cast<uintptr_t>(a.bytes);
+  };
+  for (size_t i = 0; i < outputs.size(); ++i) {
+    for (const auto& in : inputs)
+      if (overlap(outputs[i], in))
+        return set_error(T2V_ERR_INVALID_ARG, std::string(outputs[i].name) + " overlaps input " + in.name);
+    for (size_t j = i + 1; j < outputs.size(); ++j)
+      if (overlap(outputs[i], outputs[j]))
+        return set_error(T2V_ERR_INVALID_ARG,
+                         std::string(outputs[i].name) + " overlaps output " + outputs[j].name);
+  }
+  return T2V_OK;
+}
+
+namespace {
+
+struct Group {
+  int seq, head;
+  int32_t row0, len;
+  int tiles;
+};
+
+std::vector<Group> make_groups(const int32_t* cu, int nseq, int heads, int block) {
+  std::vector<Group> g;
+  for (int s = 0; s < nseq; ++s) {
+    const int32_t L = cu[s + 1] - cu[s];
+    if (L <= 0) continue;
+    const int tiles = (L + block - 1) / block;
+    for (int h = 0; h < heads; ++h) g.push_back({s, h, cu[s], L, tiles});
+  }
+  return g;
+}
+
+void append_tiles(std::vector<Item>& out, const Group& g, int t_begin, int t_end, int block) {
+  for (int t = t_begin; t < t_end; ++t) out.push_back({g.row0, g.len, t * block, g.head});
+}
+
+}  // namespace
+
+std::vector<Item> build_worklist(const int32_t* cu, int nseq, int heads, int block, int order) {
+  std::vector<Group> groups = make_groups(cu, nseq, heads, block);
+  std::vector<Item> items;
+  size_t n = 0;
+  for (const auto& g : groups) n += g.tiles;
+  items.reserve(n);
+  if (order == T2V_ORDER_NATURAL) {
+    for (const auto& g : groups) append_tiles(items, g, 0, g.tiles, block);
+    return items;
+  }
+  // Longest clip first; ties keep pack order, so one (clip, head)'s tiles stay adjacent.
+  std::stable_sort(groups.begin(), groups.end(), [](const Group& a, const Group& b) { return a.len > b.len; });
+  // Workgroup b runs on XCD b % 8, and each XCD starts its share in increasing b.
+  // Deal whole (clip, head) groups to the least-loaded XCD that still has room, so the
+  // concurrently running tiles on one XCD read the same K/V through that XCD's L2,
+  // while every XCD carries about the same cost. Groups that fit nowhere are split.
+  std::vector<size_t> cap(kNumXcd);
+  for (int x = 0; x < kNumXcd; ++x) cap[x] = n / kNumXcd + (static_cast<size_t>(x) < n % kNumXcd ? 1 : 0);
+  std::vector<std::vector<Item>> q(kNumXcd);
+  std::vector<double> load(kNumXcd, 0.0);
+  for (const auto& g : groups) {
+    int t = 0;
+    while (t < g.tiles) {
+      const size_t want = static_cast<size_t>(g.tiles - t);
+      int best = -1;
+      for (int x = 0; x < kNumXcd; ++x)  // least-loaded XCD with room for the rest of the group
+        if (cap[x] - q[x].size() >= want && (best < 0 || load[x] < load[best])) best = x;
+      size_t take = want;
+      if (best < 0) {  // split: least-loaded XCD with any room
+        for (int x = 0; x < kNumXcd; ++x)
+          if (cap[x] > q[x].size() && (best < 0 || load[x] < load[best])) best = x;
+        take = std::min(want, cap[best] - q[best].size());
+      }
+      append_tiles(q[best], g, t, t + static_cast<int>(take), block);
+      load[best] += static_cast<double>(take) * block * g.len;
+      t += static_cast<int>(take);
+    }
+  }
+  items.resize(n);
+  for (size_t b = 0; b < n; ++b) items[b] = q[b % kNumXcd][b / kNumXcd];
+  return items;
+}
+
+void plan_makespan(const Item* items, int n, int block, int slots, double* makespan, double* lower_bound) {
+  double total = 0.0, largest = 0.0;
+  auto cost = [block](const Item& it) {
+    const int rows = std::min(block, it.len - it.tile0);
+    return static_cast<double>(rows) * it.len;
+  };
+  for (int i = 0; i < n; ++i) {
+    total += cost(items[i]);
+    largest = std::max(largest, cost(items[i]));
+  }
+  *lower_bound = slots > 0 ? std::max(total / slots, largest) : 0.0;
+  double span = 0.0;
+  const int groups = (slots % kNumXcd == 0 && slots >= kNumXcd) ? kNumXcd : 1;
+  const int per = slots / groups;
+  for (int x = 0; x < groups && per > 0; ++x) {
+    std::priority_queue<double, std::vector<double>, std::greater<double>> free_at;
+    for (int s = 0; s < per; ++s) free_at.push(0.0);
+    for (int i = x; i < n; i += groups) {
+      const double t0 = free_at.top();
+      free_at.pop();
+      free_at.push(t0 + cost(items[i]));
+    }
+    while (free_at.size() > 1) free_at.pop();
+    span = std::max(span, free_at.top());
+  }
+  *makespan = span;
+}
+
+}  // namespace t2v
+
+extern "C" {
+
+const char* t2v_last_error(void) { return t2v::last_error(); }
+
+const char* t2v_version(void) { return "libt2vattn 0.1 (gfx950)"; }
+
+int t2v_build_worklist(const int32_t* cu_seqlens, int nseq, int heads, int block, int order,
+                       int32_t* items_out, int capacity, int* n_items_out) {
+  if (n_items_out == nullptr) return t2v::set_error(T2V_ERR_INVALID_ARG, "n_items_out is NULL");
+  *n_items_out = 0;
+  if (nseq < 0 || cu_seqlens == nullptr || heads < 1 || block < 1)
+    return t2v::set_error(T2V_ERR_INVALID_ARG, "bad nseq, cu_seqlens, heads or block");
+  if (order != T2V_ORDER_NATURAL && order != T2V_ORDER_LONGEST_FIRST)
+    return t2v::set_error(T2V_ERR_INVALID_ARG, "unknown order");
+  if (cu_seqlens[0] != 0) return t2v::set_error(T2V_ERR_INVALID_ARG, "cu_seqlens[0] must be 0");
+  for (int s = 0; s < nseq; ++s)
+    if (cu_seqlens[s + 1] < cu_seqlens[s])
+      return t2v::set_error(T2V_ERR_INVALID_ARG, "cu_seqlens must be non-decreasing");
+  std::vector<t2v::Item> items = t2v::build_worklist(cu_seqlens, nseq, heads, block, order);
+  if (items.size() > static_cast<size_t>(INT32_MAX))
+    return t2v::set_error(T2V_ERR_INVALID_ARG, "too many work items");
+  *n_items_out = static_cast<int>(items.size());
+  if (items_out == nullptr) return T2V_OK;
+  if (capacity < static_cast<int>(items.size()))
+    return t2v::set_error(T2V_ERR_INVALID_ARG, "capacity too small");
+  std::memcpy(items_out, items.data(), items.size() * sizeof(t2v::Item));
+  return T2V_OK;
+}
+
+int t2v_plan_makespan(const int32_t* items, int n_items, int block, int slots, double* makespan_out,
+                      double* lower_bound_out) {
+  if ((items == nullptr && n_items > 0) || n_items < 0 || block < 1 || slots < 1 || makespan_out == nullptr ||
+      lower_bound_out == nullptr)
+    return t2v::set_error(T2V_ERR_INVALID_ARG, "bad plan arguments");
+  t2v::plan_makespan(reinterpret_cast<const t2v::Item*>(items), n_items, block, slots, makespan_out,
+                     lower_bound_out);
+  return T2V_OK;
+}
+
+}  // extern "C"

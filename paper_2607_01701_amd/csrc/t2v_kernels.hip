@@ -1,0 +1,648 @@
+// gfx950 kernels for packed variable-length bidirectional attention.
+//
+// One workgroup = 4 waves = 256 threads, one work item (a tile of one clip and one
+// head, from the host scheduler). All products use v_mfma_f32_32x32x16_bf16 with fp32
+// accumulation; K/V (forward, dQ) or Q/dO (dK/dV) tiles are staged through LDS with a
+// two-buffer pipeline: the global loads for tile t+1 are issued before the MFMA work on
+// tile t and land in the other LDS buffer after it, one barrier per tile.
+//
+// Forward (paper Section III, Observation 2: full self-attention over each clip):
+// every lane owns one query row of a 32-query block, because scores are computed
+// transposed (S^T = K Q^T), so row max/sum need one swap with the other wave half.
+// The softmax is online over 32-key steps with a lazily moved reference maximum:
+// the reference m only moves when a step's maximum exceeds it by more than kTau (in
+// log2 units), which keeps every exp2 argument <= kTau and lets most steps skip the
+// rescale of the output accumulator. The final O / l and lse = ln2 (m + log2 l) are
+// exact for any reference m, so the result is the plain softmax up to rounding.
+//
+// Backward (Fig. 1 caption: the DiT backward pass): Delta = rowsum(dO * O), then a
+// dK/dV kernel (a workgroup owns 128 keys, loops over the clip's queries) and a dQ
+// kernel (a workgroup owns a query tile, loops over the clip's keys). P is recomputed
+// from the stored lse; nothing is accumulated across workgroups, so there are no
+// atomics and results are bitwise reproducible.
+#include "t2v_device.hpp"
+#include "t2v_kernels.h"
+
+namespace t2v {
+
+namespace {
+
+constexpr int kThreads = 256;  // 4 waves
+constexpr int kPad = 8;        // bf16 elements of padding per LDS row (16 bytes)
+constexpr float kTau = 8.0f;   // lazy-rescale threshold, log2 units
+constexpr int kFwdQB = 2;      // 32-query blocks per wave, forward
+constexpr int kDqQB = 1;       // 32-query blocks per wave, dQ
+
+constexpr float kInf = __builtin_huge_valf();
+
+// ------------------------------------------------------------------------------ forward
+
+template <int D, int QB, bool NEG>
+__global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
+    const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
+    const Item* __restrict__ items, int H, int64_t T, float c, bf16* __restrict__ out,
+    float* __restrict__ lse) {
+  constexpr int KK = D / 16;  // k-steps of the head-dim contraction
+  constexpr int DB = D / 32;  // 32-wide head-dim blocks of the output
+  constexpr int BN = 64;      // keys per LDS stage
+  constexpr int LS = D + kPad;
+  constexpr int CPR = D / 8;                // 16-byte chunks per row
+  constexpr int CH = BN * CPR / kThreads;   // chunks per thread per tensor
+  __shared__ __attribute__((aligned(16))) bf16 sK[2][BN * LS];
+  __shared__ __attribute__((aligned(16))) bf16 sV[2][BN * LS];
+
+  const Item it = items[blockIdx.x];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int G = lane >> 5;
+  const int l32 = lane & 31;
+  const int L = it.len;
+  const int64_t rs = static_cast<int64_t>(H) * D;  // elements between consecutive tokens
+  const int64_t base = static_cast<int64_t>(it.row0) * rs + static_cast<int64_t>(it.head) * D;
+  const bf16* kh = k + base;
+  const bf16* vh = v + base;
+  const int q_wave0 = it.tile0 + wave * QB * 32;
+  const bool wave_active = q_wave0 < L;
+
+  bf16x8 qop[QB][KK];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const int qi = q_wave0 + qb * 32 + l32;
+    const bool ok = qi < L;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) qop[qb][kk] = load8(q + base + qi * rs + kk * 16 + G * 8, ok);
+  }
+
+  f32x16 o[QB][DB];
+  float m_run[QB], l_run[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    m_run[qb] = -kInf;
+    l_run[qb] = 0.0f;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) o[qb][db] = zero16();
+  }
+
+  u32x4 rk[CH], rv[CH];
+  auto gload = [&](int j0) {
+#pragma unroll
+    for (int i = 0; i < CH; ++i) {
+      const int ci = tid + i * kThreads;
+      const int row = ci / CPR;
+      const int col = (ci % CPR) * 8;
+      const bool ok = j0 + row < L;
+      const int64_t off = static_cast<int64_t>(j0 + row) * rs + col;
+      rk[i] = load_raw16(kh + off, ok);
+      rv[i] = load_raw16(vh + off, ok);
+    }
+  };
+  auto lstore = [&](int b) {
+#pragma unroll
+    for (int i = 0; i < CH; ++i) {
+      const int ci = tid + i * kThreads;
+      const int row = ci / CPR;
+      const int col = (ci % CPR) * 8;
+      *reinterpret_cast<u32x4*>(&sK[b][row * LS + col]) = rk[i];
+      *reinterpret_cast<u32x4*>(&sV[b][row * LS + col]) = rv[i];
+    }
+  };
+
+  const int ntiles = (L + BN - 1) / BN;
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  for (int tt = 0; tt < ntiles; ++tt) {
+    const int b = tt & 1;
+    const int j0 = tt * BN;
+    if (tt + 1 < ntiles) gload(j0 + BN);
+    if (wave_active) {
+#pragma unroll
+      for (int sub = 0; sub < BN / 32; ++sub) {
+        const int kb = sub * 32;
+        const int nvalid = L - (j0 + kb);
+        if (nvalid <= 0) break;
+        // S^T (32 keys x 32 queries per block): lane = query, register r = key.
+        f32x16 s[QB];
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) s[qb] = zero16();
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+          const bf16x8 a = lds_read8(&sK[b][(kb + l32) * LS + kk * 16 + G * 8]);
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb) s[qb] = mfma(a, qop[qb][kk], s[qb]);
+        }
+        const bool ragged = nvalid < 32;
+        bf16x8 pb[QB][2];
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+          if (ragged) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const int key = (r >> 2) * 8 + G * 4 + (r & 3);
+              if (key >= nvalid) s[qb][r] = NEG ? kInf : -kInf;
+            }
+          }
+          float mx = s[qb][0];
+#pragma unroll
+          for (int r = 1; r < 16; ++r) mx = NEG ? fminf(mx, s[qb][r]) : fmaxf(mx, s[qb][r]);
+          mx = NEG ? half_min(mx) : half_max(mx);
+          const float mblk = mx * c;  // largest scaled score of this step
+          if (__any(mblk > m_run[qb] + kTau)) {
+            const float mn = fmaxf(m_run[qb], mblk);
+            const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - mn);
+            l_run[qb] *= alpha;
+#pragma unroll
+            for (int db = 0; db < DB; ++db) o[qb][db] *= alpha;
+            m_run[qb] = mn;
+          }
+          float ls = 0.0f;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            float p = __builtin_amdgcn_exp2f(fmaf(s[qb][r], c, -m_run[qb]));
+            if (ragged) {
+              const int key = (r >> 2) * 8 + G * 4 + (r & 3);
+              p = key < nvalid ? p : 0.0f;
+            }
+            s[qb][r] = p;
+            ls += p;
+          }
+          l_run[qb] += ls;
+          pb[qb][0] = to_bf16x8(s[qb], 0);
+          pb[qb][1] = to_bf16x8(s[qb], 8);
+        }
+        // O^T += V^T P^T: the key of P element t (from register 8 hf + t) is
+        // kb + 16 hf + 8 (t / 4) + 4 G + t % 4, which is how the V operand is read.
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+#pragma unroll
+          for (int db = 0; db < DB; ++db) {
+            const bf16x8 a = lds_read_rows_operand(sV[b], LS, kb + hf * 16, db * 32, lane);
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb) o[qb][db] = mfma(a, pb[qb][hf], o[qb][db]);
+          }
+        }
+      }
+    }
+    if (tt + 1 < ntiles) lstore(b ^ 1);
+    __syncthreads();
+  }
+
+  if (wave_active) {
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      const int qi = q_wave0 + qb * 32 + l32;
+      const float lt = half_sum(l_run[qb]);
+      const float inv = 1.0f / lt;
+      if (qi < L) {
+        bf16* orow = out + base + qi * rs;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            bf16x4 w;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) w[e] = static_cast<bf16>(o[qb][db][i * 4 + e] * inv);
+            *reinterpret_cast<bf16x4*>(orow + db * 32 + i * 8 + G * 4) = w;
+          }
+        }
+        if (G == 0) lse[static_cast<int64_t>(it.head) * T + it.row0 + qi] = (m_run[qb] + __builtin_amdgcn_logf(lt)) * kLn2;
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------- backward: Delta
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void attn_bwd_pre_kernel(const bf16* __restrict__ out,
+                                                                 const bf16* __restrict__ dout, int64_t rows,
+                                                                 int H, int64_t T, float* __restrict__ delta) {
+  constexpr int LPR = D / 8;            // lanes per (token, head) row
+  constexpr int RPB = kThreads / LPR;   // rows per workgroup step
+  const int sub = threadIdx.x % LPR;
+  for (int64_t row = static_cast<int64_t>(blockIdx.x) * RPB + threadIdx.x / LPR; row < rows;
+       row += static_cast<int64_t>(gridDim.x) * RPB) {
+    const bf16x8 a = *reinterpret_cast<const bf16x8*>(out + row * D + sub * 8);
+    const bf16x8 g = *reinterpret_cast<const bf16x8*>(dout + row * D + sub * 8);
+    float acc = 0.0f;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) acc = fmaf(static_cast<float>(a[t]), static_cast<float>(g[t]), acc);
+#pragma unroll
+    for (int off = LPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, LPR);
+    if (sub == 0) {
+      const int64_t t = row / H;
+      const int64_t h = row - t * H;
+      delta[h * T + t] = acc;
+    }
+  }
+}
+
+// ------------------------------------------------------------------- backward: dK, dV
+
+template <int D>
+__global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
+    const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
+    const bf16* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ delta,
+    const Item* __restrict__ items, int H, int64_t T, float c, float scale, bf16* __restrict__ dk,
+    bf16* __restrict__ dv) {
+  constexpr int KK = D / 16;
+  constexpr int DB = D / 32;
+  constexpr int BM = 64;  // queries per LDS stage
+  constexpr int LS = D + kPad;
+  constexpr int CPR = D / 8;
+  constexpr int CH = BM * CPR / kThreads;
+  __shared__ __attribute__((aligned(16))) bf16 sQ[2][BM * LS];
+  __shared__ __attribute__((aligned(16))) bf16 sG[2][BM * LS];  // dO
+  __shared__ __attribute__((aligned(16))) float sL[2][BM];      // lse * log2(e)
+  __shared__ __attribute__((aligned(16))) float sD[2][BM];      // Delta
+
+  const Item it = items[blockIdx.x];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int G = lane >> 5;
+  const int l32 = lane & 31;
+  const int L = it.len;
+  const int64_t rs = static_cast<int64_t>(H) * D;
+  const int64_t base = static_cast<int64_t>(it.row0) * rs + static_cast<int64_t>(it.head) * D;
+  const int64_t lbase = static_cast<int64_t>(it.head) * T + it.row0;
+  const bf16* qh = q + base;
+  const bf16* gh = dout + base;
+  const int key_wave0 = it.tile0 + wave * 32;
+  const bool wave_active = key_wave0 < L;
+
+  // K and V of this wave's 32 keys, as B operands (lane = key, elements along head dim).
+  bf16x8 kop[KK], vop[KK];
+  {
+    const int kj = key_wave0 + l32;
+    const bool ok = kj < L;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      kop[kk] = load8(k + base + kj * rs + kk * 16 + G * 8, ok);
+      vop[kk] = load8(v + base + kj * rs + kk * 16 + G * 8, ok);
+    }
+  }
+  f32x16 dka[DB], dva[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    dka[db] = zero16();
+    dva[db] = zero16();
+  }
+
+  u32x4 rq[CH], rg[CH];
+  float rsc = 0.0f;
+  auto gload = [&](int i0) {
+#pragma unroll
+    for (int i = 0; i < CH; ++i) {
+      const int ci = tid + i * kThreads;
+      const int row = ci / CPR;
+      const int col = (ci % CPR) * 8;
+      const bool ok = i0 + row < L;
+      const int64_t off = static_cast<int64_t>(i0 + row) * rs + col;
+      rq[i] = load_raw16(qh + off, ok);
+      rg[i] = load_raw16(gh + off, ok);
+    }
+    // Rows past the clip get lse = Delta = 0 with zero Q and dO: their P is finite and
+    // their dS and contributions are exactly zero.
+    if (tid < BM) {
+      rsc = (i0 + tid < L) ? lse[lbase + i0 + tid] * kLog2e : 0.0f;
+    } else if (tid < 2 * BM) {
+      rsc = (i0 + tid - BM < L) ? delta[lbase + i0 + tid - BM] : 0.0f;
+    }
+  };
+  auto lstore = [&](int b) {
+#pragma unroll
+    for (int i = 0; i < CH; ++i) {
+      const int ci = tid + i * kThreads;
+      const int row = ci / CPR;
+      const int col = (ci % CPR) * 8;
+      *reinterpret_cast<u32x4*>(&sQ[b][row * LS + col]) = rq[i];
+      *reinterpret_cast<u32x4*>(&sG[b][row * LS + col]) = rg[i];
+    }
+    if (tid < BM) {
+      sL[b][tid] = rsc;
+    } else if (tid < 2 * BM) {
+      sD[b][tid - BM] = rsc;
+    }
+  };
+
+  const int ntiles = (L + BM - 1) / BM;
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  for (int tt = 0; tt < ntiles; ++tt) {
+    const int b = tt & 1;
+    const int i0 = tt * BM;
+    if (tt + 1 < ntiles) gload(i0 + BM);
+    if (wave_active) {
+#pragma unroll
+      for (int sub = 0; sub < BM / 32; ++sub) {
+        const int qs = sub * 32;
+        if (L - (i0 + qs) <= 0) break;
+        // S and dP (32 queries x 32 keys): lane = key, register r = query 8 (r/4) + 4 G + r % 4.
+        f32x16 s = zero16(), dp = zero16();
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+          const bf16x8 aq = lds_read8(&sQ[b][(qs + l32) * LS + kk * 16 + G * 8]);
+          s = mfma(aq, kop[kk], s);
+        }
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+          const bf16x8 ag = lds_read8(&sG[b][(qs + l32) * LS + kk * 16 + G * 8]);
+          dp = mfma(ag, vop[kk], dp);
+        }
+        f32x4 lv[4], dl[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          lv[i] = *reinterpret_cast<const f32x4*>(&sL[b][qs + i * 8 + G * 4]);
+          dl[i] = *reinterpret_cast<const f32x4*>(&sD[b][qs + i * 8 + G * 4]);
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[r], c, -lv[r >> 2][r & 3]));
+          s[r] = p;
+          dp[r] = p * (dp[r] - dl[r >> 2][r & 3]);
+        }
+        const bf16x8 pb[2] = {to_bf16x8(s, 0), to_bf16x8(s, 8)};
+        const bf16x8 sb[2] = {to_bf16x8(dp, 0), to_bf16x8(dp, 8)};
+        // dV += P^T dO and dK += dS^T Q, contracting over the 16 queries of half hf.
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+#pragma unroll
+          for (int db = 0; db < DB; ++db) {
+            const bf16x8 bg = lds_read_rows_operand(sG[b], LS, qs + hf * 16, db * 32, lane);
+            dva[db] = mfma(pb[hf], bg, dva[db]);
+            const bf16x8 bq = lds_read_rows_operand(sQ[b], LS, qs + hf * 16, db * 32, lane);
+            dka[db] = mfma(sb[hf], bq, dka[db]);
+          }
+        }
+      }
+    }
+    if (tt + 1 < ntiles) lstore(b ^ 1);
+    __syncthreads();
+  }
+
+  if (wave_active) {
+    // Accumulators: lane = head-dim column db*32 + l32, register r = key 8 (r/4) + 4 G + r % 4.
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int kj = key_wave0 + (r >> 2) * 8 + G * 4 + (r & 3);
+      if (kj < L) {
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          dk[base + kj * rs + db * 32 + l32] = static_cast<bf16>(dka[db][r] * scale);
+          dv[base + kj * rs + db * 32 + l32] = static_cast<bf16>(dva[db][r]);
+        }
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------------ backward: dQ
+
+template <int D, int QB>
+__global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
+    const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
+    const bf16* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ delta,
+    const Item* __restrict__ items, int H, int64_t T, float c, float scale, bf16* __restrict__ dq) {
+  constexpr int KK = D / 16;
+  constexpr int DB = D / 32;
+  constexpr int BN = 64;
+  constexpr int LS = D + kPad;
+  constexpr int CPR = D / 8;
+  constexpr int CH = BN * CPR / kThreads;
+  __shared__ __attribute__((aligned(16))) bf16 sK[2][BN * LS];
+  __shared__ __attribute__((aligned(16))) bf16 sV[2][BN * LS];
+
+  const Item it = items[blockIdx.x];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int G = lane >> 5;
+  const int l32 = lane & 31;
+  const int L = it.len;
+  const int64_t rs = static_cast<int64_t>(H) * D;
+  const int64_t base = static_cast<int64_t>(it.row0) * rs + static_cast<int64_t>(it.head) * D;
+  const int64_t lbase = static_cast<int64_t>(it.head) * T + it.row0;
+  const bf16* kh = k + base;
+  const bf16* vh = v + base;
+  const int q_wave0 = it.tile0 + wave * QB * 32;
+  const bool wave_active = q_wave0 < L;
+
+  bf16x8 qop[QB][KK], gop[QB][KK];
+  float lse2[QB], dlt[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const int qi = q_wave0 + qb * 32 + l32;
+    const bool ok = qi < L;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      qop[qb][kk] = load8(q + base + qi * rs + kk * 16 + G * 8, ok);
+      gop[qb][kk] = load8(dout + base + qi * rs + kk * 16 + G * 8, ok);
+    }
+    lse2[qb] = ok ? lse[lbase + qi] * kLog2e : 0.0f;
+    dlt[qb] = ok ? delta[lbase + qi] : 0.0f;
+  }
+  f32x16 dqa[QB][DB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+    for (int db = 0; db < DB; ++db) dqa[qb][db] = zero16();
+
+  u32x4 rk[CH], rv[CH];
+  auto gload = [&](int j0) {
+#pragma unroll
+    for (int i = 0; i < CH; ++i) {
+      const int ci = tid + i * kThreads;
+      const int row = ci / CPR;
+      const int col = (ci % CPR) * 8;
+      const bool ok = j0 + row < L;
+      const int64_t off = static_cast<int64_t>(j0 + row) * rs + col;
+      rk[i] = load_raw16(kh + off, ok);
+      rv[i] = load_raw16(vh + off, ok);
+    }
+  };
+  auto lstore = [&](int b) {
+#pragma unroll
+    for (int i = 0; i < CH; ++i) {
+      const int ci = tid + i * kThreads;
+      const int row = ci / CPR;
+      const int col = (ci % CPR) * 8;
+      *reinterpret_cast<u32x4*>(&sK[b][row * LS + col]) = rk[i];
+      *reinterpret_cast<u32x4*>(&sV[b][row * LS + col]) = rv[i];
+    }
+  };
+
+  const int ntiles = (L + BN - 1) / BN;
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  for (int tt = 0; tt < ntiles; ++tt) {
+    const int b = tt & 1;
+    const int j0 = tt * BN;
+    if (tt + 1 < ntiles) gload(j0 + BN);
+    if (wave_active) {
+#pragma unroll
+      for (int sub = 0; sub < BN / 32; ++sub) {
+        const int kb = sub * 32;
+        const int nvalid = L - (j0 + kb);
+        if (nvalid <= 0) break;
+        // S^T and dP^T (32 keys x 32 queries): lane = query, register r = key.
+        f32x16 s[QB], dp[QB];
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+          s[qb] = zero16();
+          dp[qb] = zero16();
+        }
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+          const bf16x8 a = lds_read8(&sK[b][(kb + l32) * LS + kk * 16 + G * 8]);
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb) s[qb] = mfma(a, qop[qb][kk], s[qb]);
+        }
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+          const bf16x8 a = lds_read8(&sV[b][(kb + l32) * LS + kk * 16 + G * 8]);
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb) dp[qb] = mfma(a, gop[qb][kk], dp[qb]);
+        }
+        const bool ragged = nvalid < 32;
+        bf16x8 sb[QB][2];
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            float p = __builtin_amdgcn_exp2f(fmaf(s[qb][r], c, -lse2[qb]));
+            if (ragged) {  // keys past the clip (zero K rows) must not contribute
+              const int key = (r >> 2) * 8 + G * 4 + (r & 3);
+              p = key < nvalid ? p : 0.0f;
+            }
+            s[qb][r] = p * (dp[qb][r] - dlt[qb]);
+          }
+          sb[qb][0] = to_bf16x8(s[qb], 0);
+          sb[qb][1] = to_bf16x8(s[qb], 8);
+        }
+        // dQ^T += K^T dS^T over the 16 keys of half hf.
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+#pragma unroll
+          for (int db = 0; db < DB; ++db) {
+            const bf16x8 a = lds_read_rows_operand(sK[b], LS, kb + hf * 16, db * 32, lane);
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb) dqa[qb][db] = mfma(a, sb[qb][hf], dqa[qb][db]);
+          }
+        }
+      }
+    }
+    if (tt + 1 < ntiles) lstore(b ^ 1);
+    __syncthreads();
+  }
+
+  if (wave_active) {
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      const int qi = q_wave0 + qb * 32 + l32;
+      if (qi < L) {
+        bf16* row = dq + base + qi * rs;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            bf16x4 w;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) w[e] = static_cast<bf16>(dqa[qb][db][i * 4 + e] * scale);
+            *reinterpret_cast<bf16x4*>(row + db * 32 + i * 8 + G * 4) = w;
+          }
+        }
+      }
+    }
+  }
+}
+
+}  // namespace
+
+int fwd_tile_rows(int) { return (kThreads / 64) * 32 * kFwdQB; }
+int dkdv_tile_rows(int) { return (kThreads / 64) * 32; }
+int dq_tile_rows(int) { return (kThreads / 64) * 32 * kDqQB; }
+
+hipError_t launch_fwd(const AttnArgs& a, void* out, float* lse, const Item* items, int n_items,
+                      hipStream_t stream) {
+  const float c = a.scale * kLog2e;
+  const auto* q = static_cast<const bf16*>(a.q);
+  const auto* k = static_cast<const bf16*>(a.k);
+  const auto* v = static_cast<const bf16*>(a.v);
+  auto* o = static_cast<bf16*>(out);
+  const dim3 grid(n_items), block(kThreads);
+  const bool neg = a.scale < 0.0f;
+  if (a.head_dim == 128) {
+    if (neg)
+      hipLaunchKernelGGL((attn_fwd_kernel<128, kFwdQB, true>), grid, block, 0, stream, q, k, v, items, a.heads,
+                         a.total_tokens, c, o, lse);
+    else
+      hipLaunchKernelGGL((attn_fwd_kernel<128, kFwdQB, false>), grid, block, 0, stream, q, k, v, items, a.heads,
+                         a.total_tokens, c, o, lse);
+  } else {
+    if (neg)
+      hipLaunchKernelGGL((attn_fwd_kernel<64, kFwdQB, true>), grid, block, 0, stream, q, k, v, items, a.heads,
+                         a.total_tokens, c, o, lse);
+    else
+      hipLaunchKernelGGL((attn_fwd_kernel<64, kFwdQB, false>), grid, block, 0, stream, q, k, v, items, a.heads,
+                         a.total_tokens, c, o, lse);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_pre(const AttnArgs& a, hipStream_t stream) {
+  const int64_t rows = a.total_tokens * a.heads;
+  const int lpr = a.head_dim / 8;
+  const int64_t rpb = kThreads / lpr;
+  const int64_t want = (rows + rpb - 1) / rpb;
+  const dim3 grid(static_cast<unsigned>(want < 8192 ? want : 8192)), block(kThreads);
+  const auto* o = static_cast<const bf16*>(a.out);
+  const auto* g = static_cast<const bf16*>(a.dout);
+  if (a.head_dim == 128)
+    hipLaunchKernelGGL((attn_bwd_pre_kernel<128>), grid, block, 0, stream, o, g, rows, a.heads, a.total_tokens,
+                       a.delta);
+  else
+    hipLaunchKernelGGL((attn_bwd_pre_kernel<64>), grid, block, 0, stream, o, g, rows, a.heads, a.total_tokens,
+                       a.delta);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_dkdv(const AttnArgs& a, const Item* items, int n_items, hipStream_t stream) {
+  const float c = a.scale * kLog2e;
+  const dim3 grid(n_items), block(kThreads);
+  const auto* q = static_cast<const bf16*>(a.q);
+  const auto* k = static_cast<const bf16*>(a.k);
+  const auto* v = static_cast<const bf16*>(a.v);
+  const auto* g = static_cast<const bf16*>(a.dout);
+  auto* dk = static_cast<bf16*>(a.dk);
+  auto* dv = static_cast<bf16*>(a.dv);
+  if (a.head_dim == 128)
+    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<128>), grid, block, 0, stream, q, k, v, g, a.lse, a.delta, items,
+                       a.heads, a.total_tokens, c, a.scale, dk, dv);
+  else
+    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<64>), grid, block, 0, stream, q, k, v, g, a.lse, a.delta, items,
+                       a.heads, a.total_tokens, c, a.scale, dk, dv);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_dq(const AttnArgs& a, const Item* items, int n_items, hipStream_t stream) {
+  const float c = a.scale * kLog2e;
+  const dim3 grid(n_items), block(kThreads);
+  const auto* q = static_cast<const bf16*>(a.q);
+  const auto* k = static_cast<const bf16*>(a.k);
+  const auto* v = static_cast<const bf16*>(a.v);
+  const auto* g = static_cast<const bf16*>(a.dout);
+  auto* dq = static_cast<bf16*>(a.dq);
+  if (a.head_dim == 128)
+    hipLaunchKernelGGL((attn_bwd_dq_kernel<128, kDqQB>), grid, block, 0, stream, q, k, v, g, a.lse, a.delta,
+                       items, a.heads, a.total_tokens, c, a.scale, dq);
+  else
+    hipLaunchKernelGGL((attn_bwd_dq_kernel<64, kDqQB>), grid, block, 0, stream, q, k, v, g, a.lse, a.delta,
+                       items, a.heads, a.total_tokens, c, a.scale, dq);
+  return hipGetLastError();
+}
+
+}  // namespace t2v

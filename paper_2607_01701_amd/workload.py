@@ -5,16 +5,22 @@ counts from latent grids (frames x height x width patches, one clip = one
 sequence, Section III Observation 2), the pack order, and q/k/v/dout values.
 Both the HIP path and the float64 oracle consume what it returns.
 
-Value recipe: every tensor is float32 N(0, 1) from ``numpy.random.default_rng``,
-rounded to bfloat16 with round-to-nearest-even. The draw order is fixed:
-(1) clip lengths, (2) pack-order permutation, (3) q, k, v, dout.
+Value recipe: every tensor is float32 N(0, 1), rounded to bfloat16 with
+round-to-nearest-even. Shapes come from ``numpy.random.default_rng(seed)``:
+(1) clip lengths, (2) pack-order permutation. Tensor values come from
+``numpy.random.SeedSequence(seed)``: child i of four is q, k, v, dout in that
+order, and each tensor's flattened elements are cut into fixed chunks of
+2^22 values, chunk c drawn from child c of that tensor's sequence. The result
+does not depend on how many threads draw the chunks.
 The paper's datasets (WebVid, Koala, internal Lynx) are not available; these
 shapes stand in for them.
 """
 from __future__ import annotations
 
+import concurrent.futures as cf
 import dataclasses
 import math
+import os
 
 import numpy as np
 
@@ -58,19 +64,14 @@ class Pack:
         return bf16_bits_to_f32(getattr(self, name))
 
 
-def f32_to_bf16_bits(x: np.ndarray, chunk: int = 1 << 24) -> np.ndarray:
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     """Round float32 to bfloat16 (round-to-nearest-even), returning uint16 bits.
 
-    Inputs are finite normal draws, so NaN handling is not needed.
+    Inputs are finite, so the 32-bit sum below cannot overflow.
     """
-    x = np.ascontiguousarray(x, dtype=np.float32)
-    flat = x.reshape(-1).view(np.uint32)
-    out = np.empty(flat.shape, dtype=np.uint16)
-    for s in range(0, flat.size, chunk):
-        u = flat[s:s + chunk].astype(np.uint64)
-        r = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
-        out[s:s + chunk] = r.astype(np.uint16)
-    return out.reshape(x.shape)
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
+    return r.astype(np.uint16)
 
 
 def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
@@ -88,19 +89,33 @@ def cu_from_lengths(lengths) -> np.ndarray:
     return cu.astype(np.int32)
 
 
-def _draw_tensors(rng: np.random.Generator, shape, n: int = 4, chunk_rows: int = 4096):
-    """Draw n float32 N(0,1) tensors of ``shape`` in order, each rounded to bf16."""
-    outs = []
-    T = shape[0]
-    for _ in range(n):
-        t = np.empty(shape, dtype=np.uint16)
-        # One draw per tensor in row chunks: the stream is identical to a single
-        # standard_normal(shape) call because numpy fills C-order sequentially.
-        for r0 in range(0, T, chunk_rows):
-            r1 = min(T, r0 + chunk_rows)
-            t[r0:r1] = f32_to_bf16_bits(rng.standard_normal((r1 - r0,) + tuple(shape[1:]), dtype=np.float32))
-        outs.append(t)
-    return outs
+CHUNK = 1 << 22
+_THREADS = min(16, os.cpu_count() or 1)
+
+
+def _draw_tensor(ss: np.random.SeedSequence, shape) -> np.ndarray:
+    n = int(np.prod(shape))
+    out = np.empty(n, dtype=np.uint16)
+    nchunks = (n + CHUNK - 1) // CHUNK
+    children = ss.spawn(nchunks)
+
+    def fill(c):
+        a, b = c * CHUNK, min(n, (c + 1) * CHUNK)
+        x = np.random.default_rng(children[c]).standard_normal(b - a, dtype=np.float32)
+        out[a:b] = f32_to_bf16_bits(x)
+
+    if nchunks <= 1:
+        for c in range(nchunks):
+            fill(c)
+    else:
+        with cf.ThreadPoolExecutor(_THREADS) as ex:
+            list(ex.map(fill, range(nchunks)))
+    return out.reshape(shape)
+
+
+def _draw_tensors(seed: int, shape):
+    """q, k, v, dout for ``shape``: four independent streams of the seed."""
+    return [_draw_tensor(ss, shape) for ss in np.random.SeedSequence(seed).spawn(4)]
 
 
 WORKLOADS = ("tiny", "uniform", "hetero", "long", "skew")
@@ -143,18 +158,17 @@ def make_workload(name: str, seed: int = 0, tensors: bool = True) -> Pack:
     cu = cu_from_lengths(lengths)
     pack = Pack(name=name, cu_seqlens=cu, heads=H, head_dim=D, scale=1.0 / math.sqrt(D))
     if tensors:
-        pack.q, pack.k, pack.v, pack.dout = _draw_tensors(rng, (int(cu[-1]), H, D))
+        pack.q, pack.k, pack.v, pack.dout = _draw_tensors(seed, (int(cu[-1]), H, D))
     return pack
 
 
 def make_pack(lengths, heads: int, head_dim: int, seed: int = 0, scale: float | None = None,
               name: str = "custom") -> Pack:
     """A pack with explicit clip lengths (zero-length clips allowed), drawn from ``seed``."""
-    rng = np.random.default_rng(seed)
     cu = cu_from_lengths(lengths)
     sc = 1.0 / math.sqrt(head_dim) if scale is None else float(scale)
     pack = Pack(name=name, cu_seqlens=cu, heads=heads, head_dim=head_dim, scale=sc)
-    pack.q, pack.k, pack.v, pack.dout = _draw_tensors(rng, (int(cu[-1]), heads, head_dim))
+    pack.q, pack.k, pack.v, pack.dout = _draw_tensors(seed, (int(cu[-1]), heads, head_dim))
     return pack
 
 

@@ -1,0 +1,133 @@
+"""C ABI on the CPU: the libraries load, export every declared symbol, and reject bad
+arguments before anything is launched. No compute call is made here (no GPU); tensor
+pointers are fake addresses that validation never dereferences."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2607_01701_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "t2vattn.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(t2v_\w+)\s*\(", src)))
+
+
+def test_header_declares_the_abi():
+    names = declared_functions()
+    for n in ("t2v_attn_fwd", "t2v_attn_bwd", "t2v_last_error", "t2v_release_cache", "t2v_build_worklist"):
+        assert n in names
+    assert set(names) == set(_lib.EXPORTS)
+
+
+def test_hip_library_exports_every_symbol():
+    L = _lib.lib()
+    for n in declared_functions():
+        assert hasattr(L, n), n
+    assert "gfx950" in _lib.t2v_version(L)
+
+
+def test_host_library_exports():
+    L = _lib.host_lib()
+    for n in _lib.HOST_EXPORTS:
+        assert hasattr(L, n), n
+
+
+A = 0x100000  # fake, 16-byte aligned, never dereferenced
+MB = 1 << 20
+
+
+def fwd(cu, nseq=None, heads=2, head_dim=128, scale=0.125, q=A, k=A + 64 * MB, v=A + 128 * MB,
+        out=A + 192 * MB, lse=A + 256 * MB):
+    cu = np.asarray(cu, dtype=np.int32)
+    nseq = cu.shape[0] - 1 if nseq is None else nseq
+    L = _lib.lib()
+    st = L.t2v_attn_fwd(q, k, v, cu.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), nseq, heads, head_dim, scale,
+                        out, lse, None)
+    return st, _lib.t2v_last_error(L)
+
+
+def bwd(cu, **kw):
+    cu = np.asarray(cu, dtype=np.int32)
+    p = dict(q=A, k=A + 64 * MB, v=A + 128 * MB, out=A + 192 * MB, lse=A + 256 * MB, dout=A + 320 * MB,
+             dq=A + 384 * MB, dk=A + 448 * MB, dv=A + 512 * MB, delta=A + 576 * MB, heads=2, head_dim=128,
+             scale=0.125)
+    p.update(kw)
+    L = _lib.lib()
+    st = L.t2v_attn_bwd(p["q"], p["k"], p["v"], p["out"], p["lse"],
+                        cu.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), cu.shape[0] - 1, p["heads"],
+                        p["head_dim"], p["scale"], p["dout"], p["dq"], p["dk"], p["dv"], p["delta"], None)
+    return st, _lib.t2v_last_error(L)
+
+
+INV, UNS = _lib.T2V_ERR_INVALID_ARG, _lib.T2V_ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("cu,kw,status,msg", [
+    ([1, 5], {}, INV, "cu_seqlens[0]"),
+    ([0, 5, 3], {}, INV, "non-decreasing"),
+    ([0, 5], {"nseq": -1}, INV, "nseq"),
+    ([0, 5], {"heads": 0}, INV, "heads"),
+    ([0, 5], {"head_dim": 96}, UNS, "head_dim"),
+    ([0, 5], {"head_dim": 256}, UNS, "head_dim"),
+    ([0, 5], {"scale": float("nan")}, INV, "scale"),
+    ([0, 5], {"scale": float("inf")}, INV, "scale"),
+    ([0, 5], {"q": 0}, INV, "q is NULL"),
+    ([0, 5], {"lse": 0}, INV, "lse is NULL"),
+    ([0, 5], {"k": A + 64 * MB + 8}, INV, "aligned"),
+    ([0, 5], {"out": A}, INV, "overlaps"),
+    ([0, 5], {"lse": A + 128 * MB + 16}, INV, "overlaps"),
+    ([0, 5], {"heads": 1 << 21}, INV, "too large"),
+])
+def test_fwd_validation(cu, kw, status, msg):
+    st, err = fwd(cu, **kw)
+    assert st == status, err
+    assert msg in err
+
+
+def test_fwd_cu_null():
+    L = _lib.lib()
+    st = L.t2v_attn_fwd(A, A + MB, A + 2 * MB, None, 1, 2, 128, 0.1, A + 3 * MB, A + 4 * MB, None)
+    assert st == INV
+
+
+def test_fwd_empty_is_ok_without_launch():
+    # T = 0: nothing to do, no HIP call is needed, pointers may even be NULL.
+    st, _ = fwd([0, 0, 0], q=0, k=0, v=0, out=0, lse=0)
+    assert st == _lib.T2V_OK
+    st, _ = fwd([0], q=0, k=0, v=0, out=0, lse=0)
+    assert st == _lib.T2V_OK
+
+
+@pytest.mark.parametrize("kw,msg", [
+    ({"dq": A + 448 * MB}, "overlaps"),        # dq aliases dk
+    ({"dv": A}, "overlaps"),                   # dv aliases q
+    ({"delta": A + 256 * MB}, "overlaps"),     # delta aliases lse
+    ({"dout": 0}, "dout is NULL"),
+    ({"delta": 0}, "delta_ws is NULL"),
+    ({"dk": A + 448 * MB + 2}, "aligned"),
+    ({"head_dim": 32}, "head_dim"),
+])
+def test_bwd_validation(kw, msg):
+    st, err = bwd([0, 7, 20], **kw)
+    assert st in (INV, UNS), err
+    assert msg in err
+
+
+def test_bwd_empty_is_ok():
+    st, _ = bwd([0, 0], q=0, k=0, v=0, out=0, lse=0, dout=0, dq=0, dk=0, dv=0, delta=0)
+    assert st == _lib.T2V_OK
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(_lib, "_lib", None)
+    monkeypatch.setattr(_lib, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(ImportError):
+        _lib.lib()

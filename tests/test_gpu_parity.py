@@ -1,0 +1,139 @@
+"""HIP path vs the float64 oracle, element by element, on seeded packs small enough for
+the full oracle (several tiles, ragged tails, degenerate clips), plus structural
+properties: determinism, pack-order independence, clip isolation, closed forms."""
+import math
+import zlib
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_01701_amd.workload import make_pack, make_workload
+
+from gpu_util import assert_within, compare_full, dev_inputs, log, run_hip, to_np
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def oracle_of(pack, scale=None):
+    sc = pack.scale if scale is None else scale
+    return oracle.attention(pack.f32("q"), pack.f32("k"), pack.f32("v"), pack.f32("dout"), pack.cu_seqlens, sc)
+
+
+PACKS = [
+    ("edge_lengths_d128", [1, 2, 63, 64, 65, 127, 128, 129, 1000], 2, 128),
+    ("edge_lengths_d64", [1, 2, 63, 64, 65, 127, 128, 129, 1000], 2, 64),
+    ("multi_tile_d128", [2000, 513, 257], 3, 128),
+    ("zero_length_clips", [0, 37, 0, 300, 0], 2, 128),
+    ("single_long_d64", [1500], 1, 64),
+]
+
+
+@pytest.mark.parametrize("name,lens,H,D", PACKS, ids=[p[0] for p in PACKS])
+def test_parity_small_packs(name, lens, H, D):
+    pack = make_pack(lens, H, D, seed=zlib.crc32(name.encode()) % 1000)
+    log(f"case {name} lens={lens} H={H} D={D}")
+    g = to_np(run_hip(pack))
+    ref = oracle_of(pack)
+    errs, _ = compare_full(g, ref, pack.cu_seqlens, name)
+    assert_within(errs)
+
+
+def test_parity_tiny_workload():
+    pack = make_workload("tiny")
+    log("case tiny workload")
+    g = to_np(run_hip(pack))
+    ref = oracle_of(pack)
+    errs, worst = compare_full(g, ref, pack.cu_seqlens, "tiny")
+    assert_within(errs)
+    for k, e in worst.items():
+        assert e <= 2e-2, (k, e)
+
+
+@pytest.mark.parametrize("scale", [-0.3, 0.0, 0.5], ids=["negative", "zero", "large"])
+def test_parity_scales(scale):
+    pack = make_pack([70, 300, 5], 2, 128, seed=21)
+    log(f"case scale={scale}")
+    g = to_np(run_hip(pack, scale=scale))
+    ref = oracle_of(pack, scale=scale)
+    errs, _ = compare_full(g, ref, pack.cu_seqlens, f"scale {scale}")
+    assert_within(errs)
+
+
+def test_empty_pack():
+    import torch
+    from paper_2607_01701_amd import attn_bwd, attn_fwd
+    log("case empty pack")
+    z = torch.empty((0, 2, 128), dtype=torch.bfloat16, device="cuda")
+    out, lse = attn_fwd(z, z, z, np.array([0, 0], dtype=np.int32), 0.1)
+    dq, dk, dv = attn_bwd(z, z, z, out, lse, z, np.array([0, 0], dtype=np.int32), 0.1)
+    torch.cuda.synchronize()
+    assert out.numel() == 0 and dq.numel() == 0
+
+
+def test_deterministic_bitwise():
+    import torch
+    pack = make_pack([700, 129, 1], 3, 128, seed=5)
+    log("case determinism")
+    d = dev_inputs(pack)
+    a = run_hip(pack, d)
+    b = run_hip(pack, d)
+    for k in a:
+        assert torch.equal(a[k], b[k]), k
+
+
+def test_pack_order_and_isolation_bitwise():
+    """Permuting clips permutes outputs bitwise; editing one clip leaves the others bitwise."""
+    import torch
+    lens = [300, 65, 1000, 1]
+    pack = make_pack(lens, 2, 128, seed=6)
+    log("case permutation/isolation")
+    base = run_hip(pack)
+    cu = pack.cu_seqlens
+    perm = [2, 3, 0, 1]
+    idx = np.concatenate([np.arange(cu[s], cu[s + 1]) for s in perm])
+    p2 = make_pack([lens[s] for s in perm], 2, 128, seed=6)
+    for n in ("q", "k", "v", "dout"):
+        setattr(p2, n, getattr(pack, n)[idx])
+    r2 = run_hip(p2)
+    tidx = torch.from_numpy(idx).cuda()
+    for k in ("out", "dq", "dk", "dv"):
+        assert torch.equal(r2[k], base[k][tidx]), k
+    assert torch.equal(r2["lse"], base["lse"][:, tidx])
+    # edit clip 1 (tokens cu[1]..cu[2]) only
+    p3 = make_pack(lens, 2, 128, seed=6)
+    p3.q = pack.q.copy()
+    p3.q[cu[1]:cu[2]] = pack.k[cu[1]:cu[2]]
+    r3 = run_hip(p3)
+    keep = torch.from_numpy(np.r_[cu[0]:cu[1], cu[2]:cu[4]]).cuda()
+    for k in ("out", "dq", "dk", "dv"):
+        assert torch.equal(r3[k][keep], base[k][keep]), k
+
+
+def test_closed_forms_on_gpu():
+    """Length-1 clips return their V row and dout as dv; identical V rows give V."""
+    pack = make_pack([1, 1, 200, 1], 2, 128, seed=7)
+    cu = pack.cu_seqlens
+    pack.v[cu[2]:cu[3]] = pack.v[cu[2]]
+    log("case closed forms")
+    g = to_np(run_hip(pack))
+    v = pack.f32("v").astype(np.float64)
+    do = pack.f32("dout").astype(np.float64)
+    for t in (0, 1, int(cu[3])):
+        assert np.array_equal(g["out"][t], v[t])
+        assert np.array_equal(g["dv"][t], do[t])
+        # exact zeros in the definition; only fp32 rounding of dP - Delta remains
+        assert np.max(np.abs(g["dq"][t])) <= 1e-4
+        assert np.max(np.abs(g["dk"][t])) <= 1e-4
+        q = pack.f32("q")[t].astype(np.float64)
+        k = pack.f32("k")[t].astype(np.float64)
+        assert np.allclose(g["lse"][:, t], pack.scale * np.sum(q * k, axis=1), atol=1e-3)
+    a, b = int(cu[2]), int(cu[3])
+    assert np.max(np.abs(g["out"][a:b] - v[a])) <= 2e-2 * np.max(np.abs(v[a]))
