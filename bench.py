@@ -1,0 +1,258 @@
+#!/usr/bin/env python3
+"""Benchmark of the hot path on one MI355X: packed varlen attention forward + backward.
+
+A step is one t2v_attn_fwd plus one t2v_attn_bwd over the whole packed batch, with all
+inputs resident in HBM. The default workload is the heterogeneous mix (16 clips drawn
+from three latent grids, 24 heads x 128). Prints one JSON line.
+
+    python bench.py [--steps 50] [--warmup 10] [--workload hetero]
+
+The FLOP count is the usual one for attention with recomputation in the backward:
+fwd = 4 H D sum(L^2), bwd = 10 H D sum(L^2), step = 14 H D sum(L^2).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "varlen attention fwd+bwd TFLOP/s and % of bf16 MFMA peak, 1×MI355X"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+KERNEL_SOURCES = ("paper_2607_01701_amd/csrc/t2v_kernels.hip", "paper_2607_01701_amd/csrc/t2v_device.hpp")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def parse_args():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="hetero", help="tiny | uniform | hetero | long | skew")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run only a plain device copy of known size (for HBM counter scaling)")
+    return ap.parse_args()
+
+
+def kernel_flops(H, D, ssq):
+    """Algorithmic work per launch of each kernel (MFMA flops, or bytes for Delta)."""
+    base = H * D * ssq
+    return {"fwd": 4 * base, "bwd_dkdv": 8 * base, "bwd_dq": 6 * base}
+
+
+def cpu_baseline(pack, budget_s: float = 15.0):
+    """The float64 oracle, untuned, on a bounded sample of the same workload's (clip, head) pairs.
+
+    The shortest clip calibrates the oracle's rate; then clips are taken longest first,
+    skipping any whose predicted time exceeds the remaining budget, cycling over heads.
+    Clips longer than 32,768 tokens are cut to their first 8,192 tokens (a shorter clip of
+    the same statistics), so the sample stays bounded.
+    """
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover
+        threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    cu = pack.cu_seqlens
+    lens = np.diff(cu).astype(np.int64)
+    q, k, v, g = (pack.f32(n) for n in ("q", "k", "v", "dout"))
+    done, flops, t_used = [], 0.0, 0.0
+
+    def run(s, h):
+        nonlocal flops, t_used
+        a = int(cu[s])
+        n = int(min(lens[s], 8192 if lens[s] > 32768 else lens[s]))
+        t0 = time.perf_counter()
+        oracle.head_forward_backward(q[a:a + n, h], k[a:a + n, h], v[a:a + n, h], g[a:a + n, h], pack.scale)
+        dt = time.perf_counter() - t0
+        t_used += dt
+        flops += 14.0 * pack.head_dim * float(n) ** 2
+        done.append((n, h))
+        return dt, 14.0 * pack.head_dim * float(n) ** 2
+
+    nz = [int(s) for s in np.argsort(lens, kind="stable") if lens[s] > 0]
+    dt, f0 = run(nz[0], 0)
+    rate = f0 / max(dt, 1e-9)
+    distinct = []
+    for s in sorted(nz, key=lambda s: -lens[s]):
+        if int(lens[s]) not in [int(lens[x]) for x in distinct]:
+            distinct.append(s)
+    h = 0
+    progress = True
+    while t_used < budget_s and progress:
+        progress = False
+        h = (h + 1) % pack.heads
+        for s in distinct:
+            n = min(lens[s], 8192 if lens[s] > 32768 else lens[s])
+            if 14.0 * pack.head_dim * float(n) ** 2 / rate <= budget_s - t_used:
+                dt, fl = run(s, h)
+                rate = fl / max(dt, 1e-9)
+                progress = True
+            if t_used >= budget_s:
+                break
+    return {"value": flops / t_used * 1e-12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "seconds": round(t_used, 3),
+            "sample": f"{len(done)} (clip tokens, head) pairs of this workload {done}; float64 numpy oracle "
+                      f"fwd+bwd, counted at the same 14*D*L^2 per pair"}
+
+
+def copy_calibration():
+    """A plain device-to-device copy of 1 GiB, 5 times, for scaling HBM byte counters."""
+    import torch
+    n = 1 << 30
+    src = torch.ones(n // 2, dtype=torch.bfloat16, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 5}), flush=True)
+
+
+def main():
+    args = parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}): this build "
+              "has no multi-GPU path; see the sharding paragraph of DESIGN.md.", file=sys.stderr, flush=True)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    if args.copy_calibration:
+        copy_calibration()
+        return
+
+    from paper_2607_01701_amd import _lib
+    from paper_2607_01701_amd.workload import DESCRIPTIONS, attention_flops, make_workload
+
+    t_gen = time.perf_counter()
+    pack = make_workload(args.workload, seed=args.seed)
+    H, D, T = pack.heads, pack.head_dim, pack.total_tokens
+    print(f"[bench] workload {args.workload}: T={T} H={H} D={D} sum(L^2)={pack.sum_sq_len} "
+          f"(generated in {time.perf_counter() - t_gen:.1f}s)", file=sys.stderr, flush=True)
+
+    def dev(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
+
+    q, k, v, g = dev(pack.q), dev(pack.k), dev(pack.v), dev(pack.dout)
+    out = torch.empty_like(q)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+    lse = torch.empty((H, T), dtype=torch.float32, device="cuda")
+    delta = torch.empty((H, T), dtype=torch.float32, device="cuda")
+    cu = np.ascontiguousarray(pack.cu_seqlens, dtype=np.int32)
+    nseq = cu.shape[0] - 1
+    L = _lib.lib()
+    stream = torch.cuda.current_stream()
+    sh = stream.cuda_stream
+    cup = cu.ctypes.data_as(_lib._i32p)
+
+    def step():
+        st = L.t2v_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), cup, nseq, H, D, pack.scale, out.data_ptr(),
+                            lse.data_ptr(), sh)
+        if st:
+            raise _lib.T2VError(st, _lib.t2v_last_error())
+        st = L.t2v_attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(), cup, nseq, H,
+                            D, pack.scale, g.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
+                            delta.data_ptr(), sh)
+        if st:
+            raise _lib.T2VError(st, _lib.t2v_last_error())
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print(f"[bench] warmup {args.warmup} steps done", file=sys.stderr, flush=True)
+
+    _lib.t2v_timing_enable(True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ktimes = _lib.t2v_kernel_times()
+    _lib.t2v_timing_enable(False)
+    ms_step = e0.elapsed_time(e1) / args.steps
+    print(f"[bench] timed {args.steps} steps: {ms_step:.3f} ms/step", file=sys.stderr, flush=True)
+
+    fl = attention_flops(pack)
+    tflops = fl["fwd_bwd"] / (ms_step * 1e-3) * 1e-12
+    avg = {name: (ms / n if n else None) for name, (ms, n) in ktimes.items()}
+    kf = kernel_flops(H, D, pack.sum_sq_len)
+    kernels = {}
+    for name, a in avg.items():
+        entry = {"avg_ms": a, "launches": ktimes[name][1]}
+        if a and name in kf:
+            entry["tflops"] = kf[name] / (a * 1e-3) * 1e-12
+        if a and name == "bwd_pre":
+            entry["gbs"] = (4.0 * T * H * D + 4.0 * T * H) / (a * 1e-3) * 1e-9
+        kernels[name] = entry
+    dominant = max((n for n in kf if avg.get(n)), key=lambda n: ktimes[n][0])
+    achieved = kernels[dominant]["tflops"]
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+        if rec.get("kernel_source_hash") == kernel_source_hash() and rec.get("workload") == args.workload:
+            traffic = rec.get("kernels", {}).get(dominant, {}).get("hbm_bytes_per_launch")
+    roofline = {"bound": "mfma", "kernel": dominant, "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
+                "algorithmic_per_launch": kf[dominant],
+                "algorithmic_note": {"fwd": "4*H*D*sum(L^2)", "bwd_dkdv": "8*H*D*sum(L^2)",
+                                     "bwd_dq": "6*H*D*sum(L^2)"}[dominant]}
+    fwd_ms = avg["fwd"]
+    bwd_ms = sum(avg[n] for n in ("bwd_pre", "bwd_dkdv", "bwd_dq") if avg.get(n))
+    res = {
+        "metric": METRIC,
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic: seeded N(0,1) values rounded to bf16; clip lengths from latent grids (no dataset)",
+        "config": {"workload": f"{args.workload}: {DESCRIPTIONS[args.workload]}", "seed": args.seed,
+                   "total_tokens": T, "heads": H, "head_dim": D, "sum_sq_len": pack.sum_sq_len,
+                   "clip_lengths": pack.lengths.tolist() if pack.nseq <= 32 else f"{pack.nseq} clips",
+                   "flop_convention": "fwd 4*H*D*sum(L^2) + bwd 10*H*D*sum(L^2)"},
+        "frac_of_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
+        "fwd_tflops": round(fl["fwd"] / (fwd_ms * 1e-3) * 1e-12, 2),
+        "bwd_tflops": round(fl["bwd"] / (bwd_ms * 1e-3) * 1e-12, 2),
+        "kernels": kernels,
+        "roofline": roofline,
+        "kernel_source_hash": kernel_source_hash(),
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the float64 oracle on a bounded sample", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = cpu_baseline(pack)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

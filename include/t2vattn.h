@@ -112,6 +112,16 @@ int t2v_build_worklist(const int32_t* cu_seqlens, int nseq, int heads, int block
 int t2v_plan_makespan(const int32_t* items, int n_items, int block, int slots,
                       double* makespan_out, double* lower_bound_out);
 
+/* Per-kernel timing, for measurement. While enabled, every kernel launch is bracketed by
+ * two HIP events recorded on the launch stream. t2v_kernel_times waits for the recorded
+ * events, returns the summed elapsed milliseconds and the launch count of each kernel since
+ * the previous read (slots: 0 forward, 1 backward Delta, 2 backward dK/dV, 3 backward dQ),
+ * and forgets them. Enabling or disabling also forgets. Calls overlapping with launches on
+ * other host threads are serialised by a mutex.
+ *   ms_out     host double[4];  counts_out host int[4] */
+int t2v_timing_enable(int on);
+int t2v_kernel_times(double* ms_out, int* counts_out);
+
 /* Library version, for diagnostics. */
 const char* t2v_version(void);
 

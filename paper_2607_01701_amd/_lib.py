@@ -28,7 +28,8 @@ ORDER_LONGEST_FIRST = 1
 
 # Symbols declared in include/t2vattn.h.
 EXPORTS = ("t2v_attn_fwd", "t2v_attn_bwd", "t2v_last_error", "t2v_release_cache", "t2v_build_worklist",
-           "t2v_plan_makespan", "t2v_version")
+           "t2v_plan_makespan", "t2v_timing_enable", "t2v_kernel_times", "t2v_version")
+KERNEL_SLOTS = ("fwd", "bwd_pre", "bwd_dkdv", "bwd_dq")
 HOST_EXPORTS = ("t2v_last_error", "t2v_build_worklist", "t2v_plan_makespan", "t2v_version")
 
 _vp = ctypes.c_void_p
@@ -62,6 +63,10 @@ def _declare(lib, full: bool):
                                      ctypes.c_float, _vp, _vp, _vp, _vp, _f32p, _vp]
         lib.t2v_release_cache.restype = None
         lib.t2v_release_cache.argtypes = []
+        lib.t2v_timing_enable.restype = ctypes.c_int
+        lib.t2v_timing_enable.argtypes = [ctypes.c_int]
+        lib.t2v_kernel_times.restype = ctypes.c_int
+        lib.t2v_kernel_times.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int)]
     return lib
 
 
@@ -123,6 +128,18 @@ def t2v_last_error(L=None) -> str:
 
 def t2v_release_cache() -> None:
     lib().t2v_release_cache()
+
+
+def t2v_timing_enable(on: bool) -> None:
+    _check(lib(), lib().t2v_timing_enable(1 if on else 0))
+
+
+def t2v_kernel_times() -> dict:
+    """{kernel: (summed ms, launches)} since the previous read."""
+    ms = (ctypes.c_double * 4)()
+    n = (ctypes.c_int * 4)()
+    _check(lib(), lib().t2v_kernel_times(ms, n))
+    return {name: (ms[i], n[i]) for i, name in enumerate(KERNEL_SLOTS)}
 
 
 def t2v_version(L=None) -> str:

@@ -1,6 +1,7 @@
 // C ABI of libt2vattn: argument validation, the device work-list cache, and launches.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cstdlib>
 #include <cstring>
 #include <list>
@@ -146,6 +147,79 @@ PlanCache& cache() {
 
 int64_t tensor_bytes(int64_t T, int heads, int head_dim) { return T * heads * head_dim * 2; }
 
+// Optional per-kernel timing: events bracket each launch while enabled.
+enum KernelSlot { kSlotFwd = 0, kSlotPre = 1, kSlotDkdv = 2, kSlotDq = 3, kNumSlots = 4 };
+
+class KernelTimer {
+ public:
+  void set_enabled(bool on) {
+    std::lock_guard<std::mutex> lock(mu_);
+    drop_locked();
+    enabled_ = on;
+  }
+  // Runs `launch` between two events on `stream` when timing is on.
+  template <typename F>
+  hipError_t run(int slot, hipStream_t stream, F&& launch) {
+    if (!enabled_.load()) return launch();
+    hipEvent_t a = nullptr, b = nullptr;
+    hipError_t e = hipEventCreate(&a);
+    if (e == hipSuccess) e = hipEventCreate(&b);
+    if (e == hipSuccess) e = hipEventRecord(a, stream);
+    if (e == hipSuccess) e = launch();
+    if (e == hipSuccess) e = hipEventRecord(b, stream);
+    if (e != hipSuccess) {
+      if (a != nullptr) (void)hipEventDestroy(a);
+      if (b != nullptr) (void)hipEventDestroy(b);
+      return e;
+    }
+    std::lock_guard<std::mutex> lock(mu_);
+    rec_.push_back({slot, a, b});
+    return hipSuccess;
+  }
+  int read(double* ms, int* counts) {
+    std::lock_guard<std::mutex> lock(mu_);
+    for (int i = 0; i < kNumSlots; ++i) {
+      ms[i] = 0.0;
+      counts[i] = 0;
+    }
+    for (const auto& r : rec_) {
+      hipError_t e = hipEventSynchronize(r.b);
+      float t = 0.0f;
+      if (e == hipSuccess) e = hipEventElapsedTime(&t, r.a, r.b);
+      if (e != hipSuccess) {
+        drop_locked();
+        return hip_fail(e, "kernel timing events");
+      }
+      ms[r.slot] += t;
+      counts[r.slot] += 1;
+    }
+    drop_locked();
+    return T2V_OK;
+  }
+
+ private:
+  struct Rec {
+    int slot;
+    hipEvent_t a, b;
+  };
+  void drop_locked() {
+    for (const auto& r : rec_) {
+      (void)hipEventSynchronize(r.b);
+      (void)hipEventDestroy(r.a);
+      (void)hipEventDestroy(r.b);
+    }
+    rec_.clear();
+  }
+  std::mutex mu_;
+  std::atomic<bool> enabled_{false};
+  std::vector<Rec> rec_;
+};
+
+KernelTimer& timer() {
+  static KernelTimer* t = new KernelTimer();
+  return *t;
+}
+
 }  // namespace
 }  // namespace t2v
 
@@ -175,7 +249,7 @@ int t2v_attn_fwd(const void* q, const void* k, const void* v, const int32_t* cu_
     a.head_dim = head_dim;
     a.total_tokens = T;
     a.scale = scale;
-    hipError_t e = launch_fwd(a, out, lse, plan->d_items, plan->n_items, s);
+    hipError_t e = timer().run(kSlotFwd, s, [&] { return launch_fwd(a, out, lse, plan->d_items, plan->n_items, s); });
     if (e != hipSuccess) return hip_fail(e, "forward kernel launch");
     return cache().mark_used(plan, s);
   } catch (const std::bad_alloc&) {
@@ -221,14 +295,14 @@ int t2v_attn_bwd(const void* q, const void* k, const void* v, const void* out, c
     a.head_dim = head_dim;
     a.total_tokens = T;
     a.scale = scale;
-    hipError_t e = launch_bwd_pre(a, s);
+    hipError_t e = timer().run(kSlotPre, s, [&] { return launch_bwd_pre(a, s); });
     if (e != hipSuccess) return hip_fail(e, "backward preprocess launch");
     if (pk->n_items > 0) {
-      e = launch_bwd_dkdv(a, pk->d_items, pk->n_items, s);
+      e = timer().run(kSlotDkdv, s, [&] { return launch_bwd_dkdv(a, pk->d_items, pk->n_items, s); });
       if (e != hipSuccess) return hip_fail(e, "dK/dV kernel launch");
     }
     if (pq->n_items > 0) {
-      e = launch_bwd_dq(a, pq->d_items, pq->n_items, s);
+      e = timer().run(kSlotDq, s, [&] { return launch_bwd_dq(a, pq->d_items, pq->n_items, s); });
       if (e != hipSuccess) return hip_fail(e, "dQ kernel launch");
     }
     if (int st = cache().mark_used(pk, s)) return st;
@@ -238,6 +312,16 @@ int t2v_attn_bwd(const void* q, const void* k, const void* v, const void* out, c
   } catch (...) {
     return set_error(T2V_ERR_INVALID_ARG, "unexpected host exception");
   }
+}
+
+int t2v_timing_enable(int on) {
+  t2v::timer().set_enabled(on != 0);
+  return T2V_OK;
+}
+
+int t2v_kernel_times(double* ms_out, int* counts_out) {
+  if (ms_out == nullptr || counts_out == nullptr) return t2v::set_error(T2V_ERR_INVALID_ARG, "NULL output");
+  return t2v::timer().read(ms_out, counts_out);
 }
 
 void t2v_release_cache(void) {
