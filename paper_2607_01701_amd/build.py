@@ -29,8 +29,10 @@ HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
 CXX = os.environ.get("CXX_HOST", shutil.which("g++") or "g++")
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-I", os.path.join(ROOT, "include"), "-Wall"]
-# Packed fp32 VALU forms are kept out of generated code.
-HIP_FLAGS = COMMON + [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# Packed fp32 VALU forms are kept out of generated code. MFMA results stay in ordinary
+# VGPRs (the softmax reads them with VALU ops), which avoids AGPR <-> VGPR copies.
+HIP_FLAGS = COMMON + [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                      "-mllvm", "-amdgpu-mfma-vgpr-form"]
 
 
 def _run(cmd, verbose):

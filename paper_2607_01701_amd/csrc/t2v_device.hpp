@@ -85,6 +85,72 @@ T2V_DEV bf16x8 lds_read_rows_operand(const bf16* tile, int stride, int row0, int
   return r;
 }
 
+// ---------------------------------------------------------------- swizzled LDS tiles
+//
+// A tile of R rows x D bf16 is stored unpadded (row stride D) with its 16-byte chunks
+// permuted within each row: logical chunk c of row r sits in slot c ^ swz(r). swz maps
+// r % 8 to a permutation of 0..7 chosen so that both access patterns are free of bank
+// conflicts: eight consecutive rows at one chunk (the 16-byte operand reads) and four
+// consecutive rows x two adjacent chunks (the transposing 8-byte reads).
+T2V_DEV int swz(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
+
+// Element offset of (row r, column col) in a swizzled tile; col % 8 is kept.
+template <int D>
+T2V_DEV int swz_off(int r, int col) {
+  return r * D + (((col >> 3) ^ swz(r)) << 3) + (col & 7);
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Asynchronous copy of rows row0 .. row0 + R - 1 of one (clip, head) into a swizzled LDS
+// tile with global_load_lds_dwordx4 (each wave instruction fills 1 KB of LDS; lane i the
+// 16 bytes at offset 16 i). Rows at or past `L` are replaced by row L - 1, so the tile only
+// ever holds finite input values; callers mask those rows. `g` points at token 0 of the
+// clip for this head; `rs` is the token stride in elements. Completion must be awaited
+// with wait_vmcnt0() before a barrier that precedes reads of the tile.
+template <int D, int R, int NTHREADS>
+T2V_DEV void tile_dma(bf16* tile, const bf16* g, int64_t rs, int row0, int L, int tid) {
+  constexpr int CPR = D / 8;          // chunks per row
+  constexpr int RPI = 64 / CPR;       // rows per wave instruction
+  constexpr int NI = R / RPI;         // wave instructions per tile
+  constexpr int NW = NTHREADS / 64;
+  static_assert(R % RPI == 0 && NI % NW == 0, "tile shape must fill whole wave instructions");
+  const int wave = tid >> 6;
+  const int lane = tid & 63;
+#pragma unroll
+  for (int i = wave; i < NI; i += NW) {
+    const int r = i * RPI + lane / CPR;
+    const int c = (lane % CPR) ^ swz(r);
+    const int gr = min(row0 + r, L - 1);
+    __builtin_amdgcn_global_load_lds(g + gr * rs + c * 8, (lds_void*)(tile + i * 512), 16, 0, 0);
+  }
+}
+
+// Waits until this thread's outstanding vector memory operations (including LDS DMA) are done.
+T2V_DEV void wait_vmcnt0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// 16-byte operand read of logical chunk `chunk` of row r from a swizzled tile.
+template <int D>
+T2V_DEV bf16x8 swz_read8(const bf16* tile, int r, int chunk) {
+  return *reinterpret_cast<const bf16x8*>(tile + r * D + ((chunk ^ swz(r)) << 3));
+}
+
+// As lds_read_rows_operand, for a swizzled tile with row stride D.
+template <int D>
+T2V_DEV bf16x8 swz_read_rows_operand(const bf16* tile, int row0, int col0, int lane) {
+  const int G = lane >> 5;
+  const int s = lane & 15;
+  const int dhalf = (lane >> 4) & 1;
+  const int r = row0 + 4 * G + (s >> 2);
+  const int col = col0 + 16 * dhalf + 4 * (s & 3);
+  bf16x4 lo = lds_read_tr4(tile + swz_off<D>(r, col));
+  bf16x4 hi = lds_read_tr4(tile + swz_off<D>(r + 8, col));
+  bf16x8 out;
+  out[0] = lo[0]; out[1] = lo[1]; out[2] = lo[2]; out[3] = lo[3];
+  out[4] = hi[0]; out[5] = hi[1]; out[6] = hi[2]; out[7] = hi[3];
+  return out;
+}
+
 // Eight fp32 to packed bf16 (round to nearest even, v_cvt_pk_bf16_f32).
 T2V_DEV bf16x8 to_bf16x8(const f32x16& x, int base) {
   bf16x8 r;

@@ -30,26 +30,121 @@ namespace {
 constexpr int kThreads = 256;  // 4 waves
 constexpr int kPad = 8;        // bf16 elements of padding per LDS row (16 bytes)
 constexpr float kTau = 8.0f;   // lazy-rescale threshold, log2 units
-constexpr int kFwdQB = 2;      // 32-query blocks per wave, forward
+constexpr int kFwdQB = 1;      // 32-query blocks per wave, forward
 constexpr int kDqQB = 1;       // 32-query blocks per wave, dQ
 
 constexpr float kInf = __builtin_huge_valf();
 
 // ------------------------------------------------------------------------------ forward
 
+// Sum / max of the 16 values of an accumulator as a balanced tree (short dependency chains).
+T2V_DEV float tree_sum16(const f32x16& x) {
+  float a[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) a[i] = x[i] + x[i + 8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) a[i] += a[i + 4];
+  return (a[0] + a[2]) + (a[1] + a[3]);
+}
+
+template <bool NEG>
+T2V_DEV float tree_ext16(const f32x16& x) {
+  float a[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) a[i] = NEG ? fminf(x[i], x[i + 8]) : fmaxf(x[i], x[i + 8]);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) a[i] = NEG ? fminf(a[i], a[i + 4]) : fmaxf(a[i], a[i + 4]);
+  const float b0 = NEG ? fminf(a[0], a[2]) : fmaxf(a[0], a[2]);
+  const float b1 = NEG ? fminf(a[1], a[3]) : fmaxf(a[1], a[3]);
+  return NEG ? fminf(b0, b1) : fmaxf(b0, b1);
+}
+
+// One 32-key step of the forward pass for QB query blocks of this wave.
+// sK/sV: the LDS stage; kb: first key of the step within the stage; nvalid: keys of the
+// step inside the clip (only read when RAGGED, where it is 1..31).
+template <int D, int QB, bool NEG, bool RAGGED>
+T2V_DEV void fwd_step(const bf16* sK, const bf16* sV, int kb, int nvalid, float c,
+                      const bf16x8 (&qop)[QB][D / 16], f32x16 (&o)[QB][D / 32], float (&m_run)[QB],
+                      float (&l_run)[QB], int lane) {
+  constexpr int KK = D / 16;
+  constexpr int DB = D / 32;
+  const int G = lane >> 5;
+  const int l32 = lane & 31;
+  // S^T (32 keys x 32 queries per block): lane = query, register r = key 8 (r/4) + 4 G + r % 4.
+  bf16x8 ka[KK];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) ka[kk] = swz_read8<D>(sK, kb + l32, 2 * kk + G);
+  f32x16 s[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) s[qb] = zero16();
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) {
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) s[qb] = mfma(ka[kk], qop[qb][kk], s[qb]);
+  }
+  // V operands are read now so their LDS latency overlaps the softmax arithmetic.
+  bf16x8 va[2][DB];
+#pragma unroll
+  for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+    for (int db = 0; db < DB; ++db) va[hf][db] = swz_read_rows_operand<D>(sV, kb + hf * 16, db * 32, lane);
+  bf16x8 pb[QB][2];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    if constexpr (RAGGED) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = (r >> 2) * 8 + G * 4 + (r & 3);
+        if (key >= nvalid) s[qb][r] = NEG ? kInf : -kInf;
+      }
+    }
+    float mx = tree_ext16<NEG>(s[qb]);
+    mx = NEG ? half_min(mx) : half_max(mx);
+    const float mblk = mx * c;  // largest scaled score of this step
+    if (__any(mblk > m_run[qb] + kTau)) {
+      const float mn = fmaxf(m_run[qb], mblk);
+      const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - mn);
+      l_run[qb] *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) o[qb][db] *= alpha;
+      m_run[qb] = mn;
+    }
+    const float nm = -m_run[qb];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      float p = __builtin_amdgcn_exp2f(fmaf(s[qb][r], c, nm));
+      if constexpr (RAGGED) {
+        const int key = (r >> 2) * 8 + G * 4 + (r & 3);
+        p = key < nvalid ? p : 0.0f;  // also covers scale = 0, where c * -inf is NaN
+      }
+      s[qb][r] = p;
+    }
+    l_run[qb] += tree_sum16(s[qb]);
+    pb[qb][0] = to_bf16x8(s[qb], 0);
+    pb[qb][1] = to_bf16x8(s[qb], 8);
+  }
+  // O^T += V^T P^T: the key of P element t (from register 8 hf + t) is
+  // kb + 16 hf + 8 (t / 4) + 4 G + t % 4, which is how the V operand is read.
+#pragma unroll
+  for (int hf = 0; hf < 2; ++hf) {
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) o[qb][db] = mfma(va[hf][db], pb[qb][hf], o[qb][db]);
+    }
+  }
+}
+
 template <int D, int QB, bool NEG>
-__global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
+__global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
     const Item* __restrict__ items, int H, int64_t T, float c, bf16* __restrict__ out,
     float* __restrict__ lse) {
   constexpr int KK = D / 16;  // k-steps of the head-dim contraction
   constexpr int DB = D / 32;  // 32-wide head-dim blocks of the output
   constexpr int BN = 64;      // keys per LDS stage
-  constexpr int LS = D + kPad;
-  constexpr int CPR = D / 8;                // 16-byte chunks per row
-  constexpr int CH = BN * CPR / kThreads;   // chunks per thread per tensor
-  __shared__ __attribute__((aligned(16))) bf16 sK[2][BN * LS];
-  __shared__ __attribute__((aligned(16))) bf16 sV[2][BN * LS];
+  __shared__ __attribute__((aligned(1024))) bf16 sK[2][BN * D];
+  __shared__ __attribute__((aligned(1024))) bf16 sV[2][BN * D];
 
   const Item it = items[blockIdx.x];
   const int tid = threadIdx.x;
@@ -64,6 +159,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
   const bf16* vh = v + base;
   const int q_wave0 = it.tile0 + wave * QB * 32;
   const bool wave_active = q_wave0 < L;
+
+  tile_dma<D, BN, kThreads>(sK[0], kh, rs, 0, L, tid);
+  tile_dma<D, BN, kThreads>(sV[0], vh, rs, 0, L, tid);
 
   bf16x8 qop[QB][KK];
 #pragma unroll
@@ -84,108 +182,32 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
     for (int db = 0; db < DB; ++db) o[qb][db] = zero16();
   }
 
-  u32x4 rk[CH], rv[CH];
-  auto gload = [&](int j0) {
-#pragma unroll
-    for (int i = 0; i < CH; ++i) {
-      const int ci = tid + i * kThreads;
-      const int row = ci / CPR;
-      const int col = (ci % CPR) * 8;
-      const bool ok = j0 + row < L;
-      const int64_t off = static_cast<int64_t>(j0 + row) * rs + col;
-      rk[i] = load_raw16(kh + off, ok);
-      rv[i] = load_raw16(vh + off, ok);
-    }
-  };
-  auto lstore = [&](int b) {
-#pragma unroll
-    for (int i = 0; i < CH; ++i) {
-      const int ci = tid + i * kThreads;
-      const int row = ci / CPR;
-      const int col = (ci % CPR) * 8;
-      *reinterpret_cast<u32x4*>(&sK[b][row * LS + col]) = rk[i];
-      *reinterpret_cast<u32x4*>(&sV[b][row * LS + col]) = rv[i];
-    }
-  };
-
   const int ntiles = (L + BN - 1) / BN;
-  gload(0);
-  lstore(0);
+  const int nfull = L / BN;  // tiles with BN keys of the clip
+  wait_vmcnt0();
   __syncthreads();
-  for (int tt = 0; tt < ntiles; ++tt) {
+  for (int tt = 0; tt < nfull; ++tt) {
     const int b = tt & 1;
-    const int j0 = tt * BN;
-    if (tt + 1 < ntiles) gload(j0 + BN);
-    if (wave_active) {
-#pragma unroll
-      for (int sub = 0; sub < BN / 32; ++sub) {
-        const int kb = sub * 32;
-        const int nvalid = L - (j0 + kb);
-        if (nvalid <= 0) break;
-        // S^T (32 keys x 32 queries per block): lane = query, register r = key.
-        f32x16 s[QB];
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) s[qb] = zero16();
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-          const bf16x8 a = lds_read8(&sK[b][(kb + l32) * LS + kk * 16 + G * 8]);
-#pragma unroll
-          for (int qb = 0; qb < QB; ++qb) s[qb] = mfma(a, qop[qb][kk], s[qb]);
-        }
-        const bool ragged = nvalid < 32;
-        bf16x8 pb[QB][2];
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) {
-          if (ragged) {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const int key = (r >> 2) * 8 + G * 4 + (r & 3);
-              if (key >= nvalid) s[qb][r] = NEG ? kInf : -kInf;
-            }
-          }
-          float mx = s[qb][0];
-#pragma unroll
-          for (int r = 1; r < 16; ++r) mx = NEG ? fminf(mx, s[qb][r]) : fmaxf(mx, s[qb][r]);
-          mx = NEG ? half_min(mx) : half_max(mx);
-          const float mblk = mx * c;  // largest scaled score of this step
-          if (__any(mblk > m_run[qb] + kTau)) {
-            const float mn = fmaxf(m_run[qb], mblk);
-            const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - mn);
-            l_run[qb] *= alpha;
-#pragma unroll
-            for (int db = 0; db < DB; ++db) o[qb][db] *= alpha;
-            m_run[qb] = mn;
-          }
-          float ls = 0.0f;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            float p = __builtin_amdgcn_exp2f(fmaf(s[qb][r], c, -m_run[qb]));
-            if (ragged) {
-              const int key = (r >> 2) * 8 + G * 4 + (r & 3);
-              p = key < nvalid ? p : 0.0f;
-            }
-            s[qb][r] = p;
-            ls += p;
-          }
-          l_run[qb] += ls;
-          pb[qb][0] = to_bf16x8(s[qb], 0);
-          pb[qb][1] = to_bf16x8(s[qb], 8);
-        }
-        // O^T += V^T P^T: the key of P element t (from register 8 hf + t) is
-        // kb + 16 hf + 8 (t / 4) + 4 G + t % 4, which is how the V operand is read.
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-#pragma unroll
-          for (int db = 0; db < DB; ++db) {
-            const bf16x8 a = lds_read_rows_operand(sV[b], LS, kb + hf * 16, db * 32, lane);
-#pragma unroll
-            for (int qb = 0; qb < QB; ++qb) o[qb][db] = mfma(a, pb[qb][hf], o[qb][db]);
-          }
-        }
-      }
+    if (tt + 1 < ntiles) {
+      tile_dma<D, BN, kThreads>(sK[b ^ 1], kh, rs, (tt + 1) * BN, L, tid);
+      tile_dma<D, BN, kThreads>(sV[b ^ 1], vh, rs, (tt + 1) * BN, L, tid);
     }
-    if (tt + 1 < ntiles) lstore(b ^ 1);
+    if (wave_active) {
+      fwd_step<D, QB, NEG, false>(sK[b], sV[b], 0, 32, c, qop, o, m_run, l_run, lane);
+      fwd_step<D, QB, NEG, false>(sK[b], sV[b], 32, 32, c, qop, o, m_run, l_run, lane);
+    }
+    wait_vmcnt0();
     __syncthreads();
+  }
+  if (nfull < ntiles && wave_active) {  // last tile, 1 .. BN-1 keys
+    const int b = nfull & 1;
+    const int rem = L - nfull * BN;
+    if (rem >= 32) {
+      fwd_step<D, QB, NEG, false>(sK[b], sV[b], 0, 32, c, qop, o, m_run, l_run, lane);
+      if (rem > 32) fwd_step<D, QB, NEG, true>(sK[b], sV[b], 32, rem - 32, c, qop, o, m_run, l_run, lane);
+    } else {
+      fwd_step<D, QB, NEG, true>(sK[b], sV[b], 0, rem, c, qop, o, m_run, l_run, lane);
+    }
   }
 
   if (wave_active) {
