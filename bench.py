@@ -160,7 +160,7 @@ def main():
     out = torch.empty_like(q)
     dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
     lse = torch.empty((H, T), dtype=torch.float32, device="cuda")
-    delta = torch.empty((H, T), dtype=torch.float32, device="cuda")
+    delta = torch.empty((2, H, T), dtype=torch.float32, device="cuda")
     cu = np.ascontiguousarray(pack.cu_seqlens, dtype=np.int32)
     nseq = cu.shape[0] - 1
     L = _lib.lib()

@@ -21,8 +21,8 @@
  *
  * Layout. Every tensor is row-major and contiguous, "THD": element (t, h, d)
  * of a [T, H, D] tensor sits at ((t * H) + h) * D + d. q, k, v, out, dout, dq,
- * dk, dv are bfloat16 (passed as void*). lse and delta_ws are float32 laid
- * out [H, T]: element (h, t) at h * T + t. T = cu_seqlens[nseq].
+ * dk, dv are bfloat16 (passed as void*). lse is float32 laid out [H, T]:
+ * element (h, t) at h * T + t; delta_ws holds two such arrays. T = cu_seqlens[nseq].
  *
  * Ownership. The caller owns every buffer. Tensor pointers are device
  * pointers; cu_seqlens is a HOST pointer (the tile scheduler runs on the
@@ -79,7 +79,8 @@ int t2v_attn_fwd(const void* q, const void* k, const void* v,
  *   out, lse   the forward outputs for the same inputs (device, read only)
  *   dout       device bf16 [T, H, D], the gradient of the loss w.r.t. out
  *   dq, dk, dv device bf16 [T, H, D], written; must not overlap each other or any input
- *   delta_ws   device fp32 [H, T], caller-owned scratch; receives Delta = rowsum(dout * out)
+ *   delta_ws   device fp32 [2, H, T], caller-owned scratch (8 * H * T bytes): receives
+ *              Delta = rowsum(dout * out) in [0] and lse * log2(e) in [1]
  *   stream     hipStream_t to launch on
  * Deterministic: no atomics; repeated calls give bitwise-equal results.
  */

@@ -216,7 +216,7 @@ def attn_bwd(q, k, v, out, lse, dout, cu_seqlens, scale: float, dq=None, dk=None
     dk = torch.empty_like(q) if dk is None else dk
     dv = torch.empty_like(q) if dv is None else dv
     if delta_ws is None:
-        delta_ws = torch.empty((H, T), dtype=torch.float32, device=q.device)
+        delta_ws = torch.empty((2, H, T), dtype=torch.float32, device=q.device)
     L = lib()
     st = L.t2v_attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
                         cu.ctypes.data_as(_i32p), cu.shape[0] - 1, H, D, float(scale), dout.data_ptr(),

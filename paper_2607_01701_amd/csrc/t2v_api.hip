@@ -271,7 +271,7 @@ int t2v_attn_bwd(const void* q, const void* k, const void* v, const void* out, c
     const int64_t lb = T * heads * 4;
     if (int st = validate_pointers(
             {{q, tb, "q"}, {k, tb, "k"}, {v, tb, "v"}, {out, tb, "out"}, {lse, lb, "lse"}, {dout, tb, "dout"}},
-            {{dq, tb, "dq"}, {dk, tb, "dk"}, {dv, tb, "dv"}, {delta_ws, lb, "delta_ws"}}))
+            {{dq, tb, "dq"}, {dk, tb, "dk"}, {dv, tb, "dv"}, {delta_ws, 2 * lb, "delta_ws"}}))
       return st;
     if (int st = check_host_pointer(cu_seqlens)) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);

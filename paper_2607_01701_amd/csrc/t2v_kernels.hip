@@ -28,7 +28,6 @@ namespace t2v {
 namespace {
 
 constexpr int kThreads = 256;  // 4 waves
-constexpr int kPad = 8;        // bf16 elements of padding per LDS row (16 bytes)
 constexpr float kTau = 8.0f;   // lazy-rescale threshold, log2 units
 constexpr int kFwdQB = 1;      // 32-query blocks per wave, forward
 constexpr int kDqQB = 1;       // 32-query blocks per wave, dQ
@@ -236,10 +235,13 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
 
 // ------------------------------------------------------------------- backward: Delta
 
+// Delta[h, t] = sum_d dO[t, h, d] O[t, h, d]  and  lse2[h, t] = lse[h, t] * log2(e).
 template <int D>
 __global__ __launch_bounds__(kThreads) void attn_bwd_pre_kernel(const bf16* __restrict__ out,
-                                                                 const bf16* __restrict__ dout, int64_t rows,
-                                                                 int H, int64_t T, float* __restrict__ delta) {
+                                                                 const bf16* __restrict__ dout,
+                                                                 const float* __restrict__ lse, int64_t rows,
+                                                                 int H, int64_t T, float* __restrict__ delta,
+                                                                 float* __restrict__ lse2) {
   constexpr int LPR = D / 8;            // lanes per (token, head) row
   constexpr int RPB = kThreads / LPR;   // rows per workgroup step
   const int sub = threadIdx.x % LPR;
@@ -256,28 +258,89 @@ __global__ __launch_bounds__(kThreads) void attn_bwd_pre_kernel(const bf16* __re
       const int64_t t = row / H;
       const int64_t h = row - t * H;
       delta[h * T + t] = acc;
+      lse2[h * T + t] = lse[h * T + t] * kLog2e;
     }
   }
 }
 
+// Asynchronous copy of 64 consecutive floats (rows row0 .. row0 + 63, clamped to L - 1)
+// into LDS, by one wave.
+T2V_DEV void rows64_dma(float* lds, const float* g, int row0, int L, int lane) {
+  const int r = min(row0 + lane, L - 1);
+  __builtin_amdgcn_global_load_lds(g + r, (lds_void*)lds, 4, 0, 0);
+}
+
 // ------------------------------------------------------------------- backward: dK, dV
+
+// One 32-query step for this wave's 32 keys. RAGGED: only the first nvalid queries of
+// the step are inside the clip (their P is forced to zero).
+template <int D, bool RAGGED>
+T2V_DEV void dkdv_step(const bf16* sQ, const bf16* sG, const float* sL2, const float* sDl, int qs, int nvalid,
+                       float c, const bf16x8 (&kop)[D / 16], const bf16x8 (&vop)[D / 16], f32x16 (&dka)[D / 32],
+                       f32x16 (&dva)[D / 32], int lane) {
+  constexpr int KK = D / 16;
+  constexpr int DB = D / 32;
+  const int G = lane >> 5;
+  const int l32 = lane & 31;
+  // S and dP (32 queries x 32 keys): lane = key, register r = query qs + 8 (r/4) + 4 G + r % 4.
+  bf16x8 aq[KK], ag[KK];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) aq[kk] = swz_read8<D>(sQ, qs + l32, 2 * kk + G);
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) ag[kk] = swz_read8<D>(sG, qs + l32, 2 * kk + G);
+  f32x16 s = zero16(), dp = zero16();
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) s = mfma(aq[kk], kop[kk], s);
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) dp = mfma(ag[kk], vop[kk], dp);
+  f32x4 lv[4], dl[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    lv[i] = *reinterpret_cast<const f32x4*>(sL2 + qs + i * 8 + G * 4);
+    dl[i] = *reinterpret_cast<const f32x4*>(sDl + qs + i * 8 + G * 4);
+  }
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    float p = __builtin_amdgcn_exp2f(fmaf(s[r], c, -lv[r >> 2][r & 3]));
+    if constexpr (RAGGED) {
+      const int qi = (r >> 2) * 8 + G * 4 + (r & 3);
+      p = qi < nvalid ? p : 0.0f;
+    }
+    s[r] = p;
+    dp[r] = p * (dp[r] - dl[r >> 2][r & 3]);
+  }
+  const bf16x8 pb[2] = {to_bf16x8(s, 0), to_bf16x8(s, 8)};
+  const bf16x8 sb[2] = {to_bf16x8(dp, 0), to_bf16x8(dp, 8)};
+  // dV += P^T dO and dK += dS^T Q, contracting over the 16 queries of half hf.
+#pragma unroll
+  for (int hf = 0; hf < 2; ++hf) {
+    bf16x8 bg[DB], bq[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      bg[db] = swz_read_rows_operand<D>(sG, qs + hf * 16, db * 32, lane);
+      bq[db] = swz_read_rows_operand<D>(sQ, qs + hf * 16, db * 32, lane);
+    }
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      dva[db] = mfma(pb[hf], bg[db], dva[db]);
+      dka[db] = mfma(sb[hf], bq[db], dka[db]);
+    }
+  }
+}
 
 template <int D>
 __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
-    const bf16* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ delta,
+    const bf16* __restrict__ dout, const float* __restrict__ lse2, const float* __restrict__ delta,
     const Item* __restrict__ items, int H, int64_t T, float c, float scale, bf16* __restrict__ dk,
     bf16* __restrict__ dv) {
   constexpr int KK = D / 16;
   constexpr int DB = D / 32;
   constexpr int BM = 64;  // queries per LDS stage
-  constexpr int LS = D + kPad;
-  constexpr int CPR = D / 8;
-  constexpr int CH = BM * CPR / kThreads;
-  __shared__ __attribute__((aligned(16))) bf16 sQ[2][BM * LS];
-  __shared__ __attribute__((aligned(16))) bf16 sG[2][BM * LS];  // dO
-  __shared__ __attribute__((aligned(16))) float sL[2][BM];      // lse * log2(e)
-  __shared__ __attribute__((aligned(16))) float sD[2][BM];      // Delta
+  __shared__ __attribute__((aligned(1024))) bf16 sQ[2][BM * D];
+  __shared__ __attribute__((aligned(1024))) bf16 sG[2][BM * D];  // dO
+  __shared__ __attribute__((aligned(16))) float sL[2][BM];       // lse * log2(e)
+  __shared__ __attribute__((aligned(16))) float sD[2][BM];       // Delta
 
   const Item it = items[blockIdx.x];
   const int tid = threadIdx.x;
@@ -291,8 +354,18 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
   const int64_t lbase = static_cast<int64_t>(it.head) * T + it.row0;
   const bf16* qh = q + base;
   const bf16* gh = dout + base;
+  const float* l2h = lse2 + lbase;
+  const float* dlh = delta + lbase;
   const int key_wave0 = it.tile0 + wave * 32;
   const bool wave_active = key_wave0 < L;
+
+  auto stage = [&](int b, int i0) {
+    tile_dma<D, BM, kThreads>(sQ[b], qh, rs, i0, L, tid);
+    tile_dma<D, BM, kThreads>(sG[b], gh, rs, i0, L, tid);
+    if (wave == 0) rows64_dma(sL[b], l2h, i0, L, lane);
+    if (wave == 1) rows64_dma(sD[b], dlh, i0, L, lane);
+  };
+  stage(0, 0);
 
   // K and V of this wave's 32 keys, as B operands (lane = key, elements along head dim).
   bf16x8 kop[KK], vop[KK];
@@ -312,97 +385,29 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
     dva[db] = zero16();
   }
 
-  u32x4 rq[CH], rg[CH];
-  float rsc = 0.0f;
-  auto gload = [&](int i0) {
-#pragma unroll
-    for (int i = 0; i < CH; ++i) {
-      const int ci = tid + i * kThreads;
-      const int row = ci / CPR;
-      const int col = (ci % CPR) * 8;
-      const bool ok = i0 + row < L;
-      const int64_t off = static_cast<int64_t>(i0 + row) * rs + col;
-      rq[i] = load_raw16(qh + off, ok);
-      rg[i] = load_raw16(gh + off, ok);
-    }
-    // Rows past the clip get lse = Delta = 0 with zero Q and dO: their P is finite and
-    // their dS and contributions are exactly zero.
-    if (tid < BM) {
-      rsc = (i0 + tid < L) ? lse[lbase + i0 + tid] * kLog2e : 0.0f;
-    } else if (tid < 2 * BM) {
-      rsc = (i0 + tid - BM < L) ? delta[lbase + i0 + tid - BM] : 0.0f;
-    }
-  };
-  auto lstore = [&](int b) {
-#pragma unroll
-    for (int i = 0; i < CH; ++i) {
-      const int ci = tid + i * kThreads;
-      const int row = ci / CPR;
-      const int col = (ci % CPR) * 8;
-      *reinterpret_cast<u32x4*>(&sQ[b][row * LS + col]) = rq[i];
-      *reinterpret_cast<u32x4*>(&sG[b][row * LS + col]) = rg[i];
-    }
-    if (tid < BM) {
-      sL[b][tid] = rsc;
-    } else if (tid < 2 * BM) {
-      sD[b][tid - BM] = rsc;
-    }
-  };
-
   const int ntiles = (L + BM - 1) / BM;
-  gload(0);
-  lstore(0);
+  const int nfull = L / BM;
+  wait_vmcnt0();
   __syncthreads();
-  for (int tt = 0; tt < ntiles; ++tt) {
+  for (int tt = 0; tt < nfull; ++tt) {
     const int b = tt & 1;
-    const int i0 = tt * BM;
-    if (tt + 1 < ntiles) gload(i0 + BM);
+    if (tt + 1 < ntiles) stage(b ^ 1, (tt + 1) * BM);
     if (wave_active) {
-#pragma unroll
-      for (int sub = 0; sub < BM / 32; ++sub) {
-        const int qs = sub * 32;
-        if (L - (i0 + qs) <= 0) break;
-        // S and dP (32 queries x 32 keys): lane = key, register r = query 8 (r/4) + 4 G + r % 4.
-        f32x16 s = zero16(), dp = zero16();
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-          const bf16x8 aq = lds_read8(&sQ[b][(qs + l32) * LS + kk * 16 + G * 8]);
-          s = mfma(aq, kop[kk], s);
-        }
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-          const bf16x8 ag = lds_read8(&sG[b][(qs + l32) * LS + kk * 16 + G * 8]);
-          dp = mfma(ag, vop[kk], dp);
-        }
-        f32x4 lv[4], dl[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          lv[i] = *reinterpret_cast<const f32x4*>(&sL[b][qs + i * 8 + G * 4]);
-          dl[i] = *reinterpret_cast<const f32x4*>(&sD[b][qs + i * 8 + G * 4]);
-        }
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(s[r], c, -lv[r >> 2][r & 3]));
-          s[r] = p;
-          dp[r] = p * (dp[r] - dl[r >> 2][r & 3]);
-        }
-        const bf16x8 pb[2] = {to_bf16x8(s, 0), to_bf16x8(s, 8)};
-        const bf16x8 sb[2] = {to_bf16x8(dp, 0), to_bf16x8(dp, 8)};
-        // dV += P^T dO and dK += dS^T Q, contracting over the 16 queries of half hf.
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-#pragma unroll
-          for (int db = 0; db < DB; ++db) {
-            const bf16x8 bg = lds_read_rows_operand(sG[b], LS, qs + hf * 16, db * 32, lane);
-            dva[db] = mfma(pb[hf], bg, dva[db]);
-            const bf16x8 bq = lds_read_rows_operand(sQ[b], LS, qs + hf * 16, db * 32, lane);
-            dka[db] = mfma(sb[hf], bq, dka[db]);
-          }
-        }
-      }
+      dkdv_step<D, false>(sQ[b], sG[b], sL[b], sD[b], 0, 32, c, kop, vop, dka, dva, lane);
+      dkdv_step<D, false>(sQ[b], sG[b], sL[b], sD[b], 32, 32, c, kop, vop, dka, dva, lane);
     }
-    if (tt + 1 < ntiles) lstore(b ^ 1);
+    wait_vmcnt0();
     __syncthreads();
+  }
+  if (nfull < ntiles && wave_active) {  // last tile, 1 .. BM-1 queries
+    const int b = nfull & 1;
+    const int rem = L - nfull * BM;
+    if (rem >= 32) {
+      dkdv_step<D, false>(sQ[b], sG[b], sL[b], sD[b], 0, 32, c, kop, vop, dka, dva, lane);
+      if (rem > 32) dkdv_step<D, true>(sQ[b], sG[b], sL[b], sD[b], 32, rem - 32, c, kop, vop, dka, dva, lane);
+    } else {
+      dkdv_step<D, true>(sQ[b], sG[b], sL[b], sD[b], 0, rem, c, kop, vop, dka, dva, lane);
+    }
   }
 
   if (wave_active) {
@@ -423,19 +428,80 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
 
 // ------------------------------------------------------------------------ backward: dQ
 
+// One 32-key step for this wave's QB query blocks. RAGGED: only the first nvalid keys of
+// the step are inside the clip.
+template <int D, int QB, bool RAGGED>
+T2V_DEV void dq_step(const bf16* sK, const bf16* sV, int kb, int nvalid, float c, const bf16x8 (&qop)[QB][D / 16],
+                     const bf16x8 (&gop)[QB][D / 16], const float (&nl2)[QB], const float (&dlt)[QB],
+                     f32x16 (&dqa)[QB][D / 32], int lane) {
+  constexpr int KK = D / 16;
+  constexpr int DB = D / 32;
+  const int G = lane >> 5;
+  const int l32 = lane & 31;
+  // S^T and dP^T (32 keys x 32 queries): lane = query, register r = key kb + 8 (r/4) + 4 G + r % 4.
+  f32x16 s[QB], dp[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    s[qb] = zero16();
+    dp[qb] = zero16();
+  }
+  {
+    bf16x8 ka[KK];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) ka[kk] = swz_read8<D>(sK, kb + l32, 2 * kk + G);
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) s[qb] = mfma(ka[kk], qop[qb][kk], s[qb]);
+  }
+  {
+    bf16x8 va[KK];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) va[kk] = swz_read8<D>(sV, kb + l32, 2 * kk + G);
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) dp[qb] = mfma(va[kk], gop[qb][kk], dp[qb]);
+  }
+  bf16x8 kt[2][DB];
+#pragma unroll
+  for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+    for (int db = 0; db < DB; ++db) kt[hf][db] = swz_read_rows_operand<D>(sK, kb + hf * 16, db * 32, lane);
+  bf16x8 sb[QB][2];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      float p = __builtin_amdgcn_exp2f(fmaf(s[qb][r], c, nl2[qb]));
+      if constexpr (RAGGED) {  // keys past the clip must not contribute
+        const int key = (r >> 2) * 8 + G * 4 + (r & 3);
+        p = key < nvalid ? p : 0.0f;
+      }
+      s[qb][r] = p * (dp[qb][r] - dlt[qb]);
+    }
+    sb[qb][0] = to_bf16x8(s[qb], 0);
+    sb[qb][1] = to_bf16x8(s[qb], 8);
+  }
+  // dQ^T += K^T dS^T over the 16 keys of half hf.
+#pragma unroll
+  for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) dqa[qb][db] = mfma(kt[hf][db], sb[qb][hf], dqa[qb][db]);
+}
+
 template <int D, int QB>
-__global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
+__global__ __launch_bounds__(kThreads, 2) void attn_bwd_dq_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
-    const bf16* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ delta,
+    const bf16* __restrict__ dout, const float* __restrict__ lse2, const float* __restrict__ delta,
     const Item* __restrict__ items, int H, int64_t T, float c, float scale, bf16* __restrict__ dq) {
   constexpr int KK = D / 16;
   constexpr int DB = D / 32;
   constexpr int BN = 64;
-  constexpr int LS = D + kPad;
-  constexpr int CPR = D / 8;
-  constexpr int CH = BN * CPR / kThreads;
-  __shared__ __attribute__((aligned(16))) bf16 sK[2][BN * LS];
-  __shared__ __attribute__((aligned(16))) bf16 sV[2][BN * LS];
+  __shared__ __attribute__((aligned(1024))) bf16 sK[2][BN * D];
+  __shared__ __attribute__((aligned(1024))) bf16 sV[2][BN * D];
 
   const Item it = items[blockIdx.x];
   const int tid = threadIdx.x;
@@ -452,8 +518,11 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
   const int q_wave0 = it.tile0 + wave * QB * 32;
   const bool wave_active = q_wave0 < L;
 
+  tile_dma<D, BN, kThreads>(sK[0], kh, rs, 0, L, tid);
+  tile_dma<D, BN, kThreads>(sV[0], vh, rs, 0, L, tid);
+
   bf16x8 qop[QB][KK], gop[QB][KK];
-  float lse2[QB], dlt[QB];
+  float nl2[QB], dlt[QB];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const int qi = q_wave0 + qb * 32 + l32;
@@ -463,7 +532,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
       qop[qb][kk] = load8(q + base + qi * rs + kk * 16 + G * 8, ok);
       gop[qb][kk] = load8(dout + base + qi * rs + kk * 16 + G * 8, ok);
     }
-    lse2[qb] = ok ? lse[lbase + qi] * kLog2e : 0.0f;
+    nl2[qb] = ok ? -lse2[lbase + qi] : 0.0f;
     dlt[qb] = ok ? delta[lbase + qi] : 0.0f;
   }
   f32x16 dqa[QB][DB];
@@ -472,93 +541,32 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dq_kernel(
 #pragma unroll
     for (int db = 0; db < DB; ++db) dqa[qb][db] = zero16();
 
-  u32x4 rk[CH], rv[CH];
-  auto gload = [&](int j0) {
-#pragma unroll
-    for (int i = 0; i < CH; ++i) {
-      const int ci = tid + i * kThreads;
-      const int row = ci / CPR;
-      const int col = (ci % CPR) * 8;
-      const bool ok = j0 + row < L;
-      const int64_t off = static_cast<int64_t>(j0 + row) * rs + col;
-      rk[i] = load_raw16(kh + off, ok);
-      rv[i] = load_raw16(vh + off, ok);
-    }
-  };
-  auto lstore = [&](int b) {
-#pragma unroll
-    for (int i = 0; i < CH; ++i) {
-      const int ci = tid + i * kThreads;
-      const int row = ci / CPR;
-      const int col = (ci % CPR) * 8;
-      *reinterpret_cast<u32x4*>(&sK[b][row * LS + col]) = rk[i];
-      *reinterpret_cast<u32x4*>(&sV[b][row * LS + col]) = rv[i];
-    }
-  };
-
   const int ntiles = (L + BN - 1) / BN;
-  gload(0);
-  lstore(0);
+  const int nfull = L / BN;
+  wait_vmcnt0();
   __syncthreads();
-  for (int tt = 0; tt < ntiles; ++tt) {
+  for (int tt = 0; tt < nfull; ++tt) {
     const int b = tt & 1;
-    const int j0 = tt * BN;
-    if (tt + 1 < ntiles) gload(j0 + BN);
-    if (wave_active) {
-#pragma unroll
-      for (int sub = 0; sub < BN / 32; ++sub) {
-        const int kb = sub * 32;
-        const int nvalid = L - (j0 + kb);
-        if (nvalid <= 0) break;
-        // S^T and dP^T (32 keys x 32 queries): lane = query, register r = key.
-        f32x16 s[QB], dp[QB];
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) {
-          s[qb] = zero16();
-          dp[qb] = zero16();
-        }
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-          const bf16x8 a = lds_read8(&sK[b][(kb + l32) * LS + kk * 16 + G * 8]);
-#pragma unroll
-          for (int qb = 0; qb < QB; ++qb) s[qb] = mfma(a, qop[qb][kk], s[qb]);
-        }
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-          const bf16x8 a = lds_read8(&sV[b][(kb + l32) * LS + kk * 16 + G * 8]);
-#pragma unroll
-          for (int qb = 0; qb < QB; ++qb) dp[qb] = mfma(a, gop[qb][kk], dp[qb]);
-        }
-        const bool ragged = nvalid < 32;
-        bf16x8 sb[QB][2];
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) {
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            float p = __builtin_amdgcn_exp2f(fmaf(s[qb][r], c, -lse2[qb]));
-            if (ragged) {  // keys past the clip (zero K rows) must not contribute
-              const int key = (r >> 2) * 8 + G * 4 + (r & 3);
-              p = key < nvalid ? p : 0.0f;
-            }
-            s[qb][r] = p * (dp[qb][r] - dlt[qb]);
-          }
-          sb[qb][0] = to_bf16x8(s[qb], 0);
-          sb[qb][1] = to_bf16x8(s[qb], 8);
-        }
-        // dQ^T += K^T dS^T over the 16 keys of half hf.
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-#pragma unroll
-          for (int db = 0; db < DB; ++db) {
-            const bf16x8 a = lds_read_rows_operand(sK[b], LS, kb + hf * 16, db * 32, lane);
-#pragma unroll
-            for (int qb = 0; qb < QB; ++qb) dqa[qb][db] = mfma(a, sb[qb][hf], dqa[qb][db]);
-          }
-        }
-      }
+    if (tt + 1 < ntiles) {
+      tile_dma<D, BN, kThreads>(sK[b ^ 1], kh, rs, (tt + 1) * BN, L, tid);
+      tile_dma<D, BN, kThreads>(sV[b ^ 1], vh, rs, (tt + 1) * BN, L, tid);
     }
-    if (tt + 1 < ntiles) lstore(b ^ 1);
+    if (wave_active) {
+      dq_step<D, QB, false>(sK[b], sV[b], 0, 32, c, qop, gop, nl2, dlt, dqa, lane);
+      dq_step<D, QB, false>(sK[b], sV[b], 32, 32, c, qop, gop, nl2, dlt, dqa, lane);
+    }
+    wait_vmcnt0();
     __syncthreads();
+  }
+  if (nfull < ntiles && wave_active) {
+    const int b = nfull & 1;
+    const int rem = L - nfull * BN;
+    if (rem >= 32) {
+      dq_step<D, QB, false>(sK[b], sV[b], 0, 32, c, qop, gop, nl2, dlt, dqa, lane);
+      if (rem > 32) dq_step<D, QB, true>(sK[b], sV[b], 32, rem - 32, c, qop, gop, nl2, dlt, dqa, lane);
+    } else {
+      dq_step<D, QB, true>(sK[b], sV[b], 0, rem, c, qop, gop, nl2, dlt, dqa, lane);
+    }
   }
 
   if (wave_active) {
@@ -623,12 +631,13 @@ hipError_t launch_bwd_pre(const AttnArgs& a, hipStream_t stream) {
   const dim3 grid(static_cast<unsigned>(want < 8192 ? want : 8192)), block(kThreads);
   const auto* o = static_cast<const bf16*>(a.out);
   const auto* g = static_cast<const bf16*>(a.dout);
+  float* lse2 = a.delta + rows;
   if (a.head_dim == 128)
-    hipLaunchKernelGGL((attn_bwd_pre_kernel<128>), grid, block, 0, stream, o, g, rows, a.heads, a.total_tokens,
-                       a.delta);
+    hipLaunchKernelGGL((attn_bwd_pre_kernel<128>), grid, block, 0, stream, o, g, a.lse, rows, a.heads,
+                       a.total_tokens, a.delta, lse2);
   else
-    hipLaunchKernelGGL((attn_bwd_pre_kernel<64>), grid, block, 0, stream, o, g, rows, a.heads, a.total_tokens,
-                       a.delta);
+    hipLaunchKernelGGL((attn_bwd_pre_kernel<64>), grid, block, 0, stream, o, g, a.lse, rows, a.heads,
+                       a.total_tokens, a.delta, lse2);
   return hipGetLastError();
 }
 
@@ -641,11 +650,12 @@ hipError_t launch_bwd_dkdv(const AttnArgs& a, const Item* items, int n_items, hi
   const auto* g = static_cast<const bf16*>(a.dout);
   auto* dk = static_cast<bf16*>(a.dk);
   auto* dv = static_cast<bf16*>(a.dv);
+  const float* lse2 = a.delta + a.total_tokens * a.heads;
   if (a.head_dim == 128)
-    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<128>), grid, block, 0, stream, q, k, v, g, a.lse, a.delta, items,
+    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<128>), grid, block, 0, stream, q, k, v, g, lse2, a.delta, items,
                        a.heads, a.total_tokens, c, a.scale, dk, dv);
   else
-    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<64>), grid, block, 0, stream, q, k, v, g, a.lse, a.delta, items,
+    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<64>), grid, block, 0, stream, q, k, v, g, lse2, a.delta, items,
                        a.heads, a.total_tokens, c, a.scale, dk, dv);
   return hipGetLastError();
 }
@@ -658,11 +668,12 @@ hipError_t launch_bwd_dq(const AttnArgs& a, const Item* items, int n_items, hipS
   const auto* v = static_cast<const bf16*>(a.v);
   const auto* g = static_cast<const bf16*>(a.dout);
   auto* dq = static_cast<bf16*>(a.dq);
+  const float* lse2 = a.delta + a.total_tokens * a.heads;
   if (a.head_dim == 128)
-    hipLaunchKernelGGL((attn_bwd_dq_kernel<128, kDqQB>), grid, block, 0, stream, q, k, v, g, a.lse, a.delta,
+    hipLaunchKernelGGL((attn_bwd_dq_kernel<128, kDqQB>), grid, block, 0, stream, q, k, v, g, lse2, a.delta,
                        items, a.heads, a.total_tokens, c, a.scale, dq);
   else
-    hipLaunchKernelGGL((attn_bwd_dq_kernel<64, kDqQB>), grid, block, 0, stream, q, k, v, g, a.lse, a.delta,
+    hipLaunchKernelGGL((attn_bwd_dq_kernel<64, kDqQB>), grid, block, 0, stream, q, k, v, g, lse2, a.delta,
                        items, a.heads, a.total_tokens, c, a.scale, dq);
   return hipGetLastError();
 }

@@ -110,6 +110,7 @@ def test_fwd_empty_is_ok_without_launch():
     ({"dq": A + 448 * MB}, "overlaps"),        # dq aliases dk
     ({"dv": A}, "overlaps"),                   # dv aliases q
     ({"delta": A + 256 * MB}, "overlaps"),     # delta aliases lse
+    ({"delta": A + 320 * MB - 8 * 20}, "overlaps"),  # second half of delta_ws reaches dout
     ({"dout": 0}, "dout is NULL"),
     ({"delta": 0}, "delta_ws is NULL"),
     ({"dk": A + 448 * MB + 2}, "aligned"),
