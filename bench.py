@@ -48,6 +48,10 @@ def parse_args():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain device copy of known size (for HBM counter scaling)")
+    ap.add_argument("--ingest-rocpd", nargs=5, metavar=("KT_DB", "FETCH_DB", "WRITE_DB", "COPY_FETCH_DB",
+                                                        "COPY_WRITE_DB"),
+                    help="summarise rocprofv3 databases (kernel trace, FETCH_SIZE and WRITE_SIZE of this bench and "
+                         "of --copy-calibration) into profiles/; runs on the CPU")
     return ap.parse_args()
 
 
@@ -127,12 +131,77 @@ def copy_calibration():
     print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 5}), flush=True)
 
 
+SLOT_OF_KERNEL = {"attn_fwd_kernel": "fwd", "attn_bwd_pre_kernel": "bwd_pre", "attn_bwd_dkdv_kernel": "bwd_dkdv",
+                  "attn_bwd_dq_kernel": "bwd_dq"}
+
+
+def _slot(name):
+    for key, slot in SLOT_OF_KERNEL.items():
+        if key in name:
+            return slot
+    return None
+
+
+def ingest_rocpd(kt_db, fetch_db, write_db, copy_fetch_db, copy_write_db, workload):
+    """Per-kernel durations and HBM bytes from rocprofv3 (rocpd SQLite) output.
+
+    FETCH_SIZE / WRITE_SIZE are scaled by what they read for a plain copy of known size.
+    Writes profiles/hbm_traffic.json (read by the bench) and prints a text summary.
+    """
+    import sqlite3
+
+    def counters(db):
+        c = sqlite3.connect(db)
+        rows = c.execute("select kernel_name, counter_name, count(*), avg(value) from counters_collection "
+                         "group by kernel_name, counter_name").fetchall()
+        c.close()
+        return rows
+
+    copy_bytes = 1 << 30
+    cf = [r for r in counters(copy_fetch_db) if "copyBuffer" in r[0]]
+    cw = [r for r in counters(copy_write_db) if "copyBuffer" in r[0]]
+    f_scale = copy_bytes / (cf[0][3] * 1024.0)
+    w_scale = copy_bytes / (cw[0][3] * 1024.0)
+    kt = sqlite3.connect(kt_db)
+    trace = kt.execute("select name, count(*), avg(end-start), min(end-start), max(end-start) from kernels "
+                       "group by name").fetchall()
+    kt.close()
+    kernels = {}
+    lines = [f"kernel-trace (ns -> ms)          launches    avg_ms     min_ms     max_ms"]
+    for name, n, avg, mn, mx in sorted(trace, key=lambda r: -r[1] * r[2]):
+        slot = _slot(name)
+        if slot:
+            kernels.setdefault(slot, {})["trace_avg_ms"] = avg / 1e6
+            lines.append(f"  {slot:28s} {n:8d} {avg / 1e6:10.4f} {mn / 1e6:10.4f} {mx / 1e6:10.4f}")
+    for rows, key, scale in ((counters(fetch_db), "fetch", f_scale), (counters(write_db), "write", w_scale)):
+        for name, cname, n, avg_kb in rows:
+            slot = _slot(name)
+            if slot:
+                kernels.setdefault(slot, {})[f"{key}_kib_raw"] = avg_kb
+                kernels[slot][f"{key}_bytes"] = avg_kb * 1024.0 * scale
+    lines.append(f"HBM counters per launch (copy-scaled: FETCH x{f_scale:.4f}, WRITE x{w_scale:.4f})")
+    for slot, k in kernels.items():
+        if "fetch_bytes" in k and "write_bytes" in k:
+            k["hbm_bytes_per_launch"] = k["fetch_bytes"] + k["write_bytes"]
+            lines.append(f"  {slot:28s} fetch {k['fetch_bytes'] / 1e9:8.3f} GB  write {k['write_bytes'] / 1e9:8.3f} GB"
+                         f"  total {k['hbm_bytes_per_launch'] / 1e9:8.3f} GB")
+    rec = {"workload": workload, "kernel_source_hash": kernel_source_hash(), "fetch_scale": f_scale,
+           "write_scale": w_scale, "copy_bytes": copy_bytes, "kernels": kernels}
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(rec, f, indent=1, sort_keys=True)
+    print("\n".join(lines))
+
+
 def main():
     args = parse_args()
+    if args.ingest_rocpd:
+        ingest_rocpd(*args.ingest_rocpd, workload=args.workload)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}): this build "
-              "has no multi-GPU path; see the sharding paragraph of DESIGN.md.", file=sys.stderr, flush=True)
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}): libt2vattn "
+              "has no multi-GPU path; sharding across GPUs is not implemented.", file=sys.stderr, flush=True)
         sys.exit(2)
     import numpy as np
     import torch
