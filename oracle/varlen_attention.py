@@ -206,3 +206,39 @@ def key_rows(q, k, v, dout, cu_seqlens, scale: float, seq: int, head: int, keys,
         dv += Pc.T @ dOb
         dk += scale * (dSc.T @ Qb)
     return {"dk": dk, "dv": dv}
+
+
+def key_rows_torch(q, k, v, dout, cu_seqlens, scale: float, seq: int, head: int, keys,
+                   block_rows: int = 2048) -> dict:
+    """``key_rows`` with torch float64 CPU tensor operations (multithreaded matmul and exp).
+
+    Same steps as ``key_rows``; used for the 75,600- and 100,800-token clips, where one
+    head's full score matrix is about 10^10 entries.
+    """
+    import torch
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    a, b = int(cu[seq]), int(cu[seq + 1])
+    kt = torch.as_tensor(np.asarray(keys, dtype=np.int64))
+
+    def t64(x):
+        return torch.as_tensor(np.ascontiguousarray(np.asarray(x[a:b, head], dtype=np.float64)))
+
+    Q, K, V, dO = t64(q), t64(k), t64(v), t64(dout)
+    L = b - a
+    Vs = V[kt]
+    dk = torch.zeros((kt.shape[0], Q.shape[1]), dtype=torch.float64)
+    dv = torch.zeros_like(dk)
+    for r0 in range(0, L, block_rows):
+        r1 = min(L, r0 + block_rows)
+        Qb, dOb = Q[r0:r1], dO[r0:r1]
+        S = scale * (Qb @ K.T)
+        m = S.max(dim=1).values
+        E = torch.exp(S - m[:, None])
+        P = E / E.sum(dim=1)[:, None]
+        Ob = P @ V
+        db = (dOb * Ob).sum(dim=1)
+        Pc = P[:, kt]
+        dSc = Pc * (dOb @ Vs.T - db[:, None])
+        dv += Pc.T @ dOb
+        dk += scale * (dSc.T @ Qb)
+    return {"dk": dk.numpy(), "dv": dv.numpy()}

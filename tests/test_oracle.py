@@ -419,3 +419,15 @@ def test_mutants_are_caught(name):
         except Exception:  # a shape error is also a detection
             failing.append(pin)
     assert failing, f"mutant {name} passed every pin"
+
+
+def test_key_rows_torch_matches_full():
+    """The torch variant of the key-column routine equals the full oracle at those keys."""
+    lens = [30, 90]
+    cu, q, k, v, do = rand_pack(lens, 2, 8, 17)
+    full = orc.attention(q, k, v, do, cu, 0.3)
+    keys = [0, 44, 89]
+    r = orc.key_rows_torch(q, k, v, do, cu, 0.3, seq=1, head=0, keys=keys, block_rows=13)
+    for i, j in enumerate(keys):
+        assert np.allclose(r["dk"][i], full["dk"][30 + j, 0], atol=1e-13)
+        assert np.allclose(r["dv"][i], full["dv"][30 + j, 0], atol=1e-13)
