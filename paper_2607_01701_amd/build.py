@@ -30,9 +30,11 @@ CXX = os.environ.get("CXX_HOST", shutil.which("g++") or "g++")
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-I", os.path.join(ROOT, "include"), "-Wall"]
 # Packed fp32 VALU forms are kept out of generated code. MFMA results stay in ordinary
-# VGPRs (the softmax reads them with VALU ops), which avoids AGPR <-> VGPR copies.
+# VGPRs (the softmax reads them with VALU ops), which avoids AGPR <-> VGPR copies. The
+# iterative ILP scheduler interleaves the LDS reads, MFMAs and softmax arithmetic of a step
+# better than the default occupancy-driven one (measured: dK/dV +19%, dQ +7%).
 HIP_FLAGS = COMMON + [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-                      "-mllvm", "-amdgpu-mfma-vgpr-form"]
+                      "-mllvm", "-amdgpu-mfma-vgpr-form", "-mllvm", "-amdgpu-sched-strategy=iterative-ilp"]
 
 
 def _run(cmd, verbose):
