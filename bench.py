@@ -26,7 +26,10 @@ if ROOT not in sys.path:
 METRIC = "varlen attention fwd+bwd TFLOP/s and % of bf16 MFMA peak, 1×MI355X"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
-KERNEL_SOURCES = ("paper_2607_01701_amd/csrc/t2v_kernels.hip", "paper_2607_01701_amd/csrc/t2v_device.hpp")
+KERNEL_SOURCES = ("paper_2607_01701_amd/csrc/t2v_fwd.hip", "paper_2607_01701_amd/csrc/t2v_bwd_pre.hip",
+                  "paper_2607_01701_amd/csrc/t2v_bwd_dkdv.hip", "paper_2607_01701_amd/csrc/t2v_bwd_dq.hip",
+                  "paper_2607_01701_amd/csrc/t2v_kernel_common.hpp", "paper_2607_01701_amd/csrc/t2v_device.hpp",
+                  "paper_2607_01701_amd/build.py")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 
 

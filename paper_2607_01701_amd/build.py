@@ -21,7 +21,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libt2vattn.so")
 HOST_LIB = os.path.join(PKG, "libt2vattn_host.so")
 
-HIP_SOURCES = ["t2v_kernels.hip", "t2v_api.hip"]
+HIP_SOURCES = ["t2v_fwd.hip", "t2v_bwd_pre.hip", "t2v_bwd_dkdv.hip", "t2v_bwd_dq.hip", "t2v_api.hip"]
 HOST_SOURCES = ["t2v_host.cpp"]
 
 ARCH = os.environ.get("T2V_OFFLOAD_ARCH", "gfx950")
@@ -30,11 +30,17 @@ CXX = os.environ.get("CXX_HOST", shutil.which("g++") or "g++")
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-I", os.path.join(ROOT, "include"), "-Wall"]
 # Packed fp32 VALU forms are kept out of generated code. MFMA results stay in ordinary
-# VGPRs (the softmax reads them with VALU ops), which avoids AGPR <-> VGPR copies. The
-# iterative ILP scheduler interleaves the LDS reads, MFMAs and softmax arithmetic of a step
-# better than the default occupancy-driven one (measured: dK/dV +19%, dQ +7%).
+# VGPRs (the softmax reads them with VALU ops), which avoids AGPR <-> VGPR copies.
 HIP_FLAGS = COMMON + [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-                      "-mllvm", "-amdgpu-mfma-vgpr-form", "-mllvm", "-amdgpu-sched-strategy=iterative-ilp"]
+                      "-mllvm", "-amdgpu-mfma-vgpr-form"]
+# Machine-scheduler strategy per kernel, chosen by measurement on MI355X: the ILP-driven
+# schedulers interleave LDS reads, MFMAs and softmax arithmetic better, but raise register
+# pressure, which only the one-workgroup-per-CU dK/dV kernel can afford in full.
+SCHED = {
+    "t2v_fwd.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"],
+    "t2v_bwd_dkdv.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-ilp"],
+    "t2v_bwd_dq.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"],
+}
 
 
 def _run(cmd, verbose):
@@ -55,12 +61,12 @@ def build(verbose: bool = True) -> None:
     for s in HIP_SOURCES:
         o = os.path.join(BUILD, s + ".o")
         objs.append(o)
-        jobs.append([HIPCC, *HIP_FLAGS, "-c", os.path.join(CSRC, s), "-o", o])
+        jobs.append([HIPCC, *HIP_FLAGS, *SCHED.get(s, []), "-c", os.path.join(CSRC, s), "-o", o])
     for s in HOST_SOURCES:
         o = os.path.join(BUILD, s + ".o")
         objs.append(o)
         jobs.append([CXX, *COMMON, "-c", os.path.join(CSRC, s), "-o", o])
-    with cf.ThreadPoolExecutor(max_workers=4) as ex:
+    with cf.ThreadPoolExecutor(max_workers=6) as ex:
         for f in [ex.submit(_run, j, verbose) for j in jobs]:
             f.result()
     tmp = LIB + ".tmp"

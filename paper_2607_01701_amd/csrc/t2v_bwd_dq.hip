@@ -1,0 +1,205 @@
+// Backward dQ kernel: a workgroup owns a query tile of one (clip, head) and loops over
+// the clip's keys; every output element is written by one lane (no atomics).
+#include "t2v_kernel_common.hpp"
+
+namespace t2v {
+
+using namespace kern;
+
+namespace {
+
+constexpr int kDqQB = 1;  // 32-query blocks per wave
+
+// ------------------------------------------------------------------------ backward: dQ
+
+// One 32-key step for this wave's QB query blocks. RAGGED: only the first nvalid keys of
+// the step are inside the clip.
+template <int D, int QB, bool RAGGED>
+T2V_DEV void dq_step(uint32_t kbase, uint32_t vbase, uint32_t kr0, uint32_t kr1, int kb, int nvalid, float c,
+                     const bf16x8 (&qop)[QB][D / 16],
+                     const bf16x8 (&gop)[QB][D / 16], const float (&nl2)[QB], const float (&dlt)[QB],
+                     f32x16 (&dqa)[QB][D / 32], int lane) {
+  constexpr int KK = D / 16;
+  constexpr int DB = D / 32;
+  const int G = lane >> 5;
+  const int l32 = lane & 31;
+  // S^T and dP^T (32 keys x 32 queries): lane = query, register r = key kb + 8 (r/4) + 4 G + r % 4.
+  f32x16 s[QB], dp[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    s[qb] = zero16();
+    dp[qb] = zero16();
+  }
+  {
+    bf16x8 ka[KK];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) ka[kk] = read_opnd<D>(kbase, kb, kk);
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) s[qb] = mfma(ka[kk], qop[qb][kk], s[qb]);
+  }
+  {
+    bf16x8 va[KK];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) va[kk] = read_opnd<D>(vbase, kb, kk);
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) dp[qb] = mfma(va[kk], gop[qb][kk], dp[qb]);
+  }
+  bf16x8 kt[2][DB];
+#pragma unroll
+  for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+    for (int db = 0; db < DB; ++db) kt[hf][db] = read_rows_opnd<D>(kr0, kr1, kb + hf * 16, db);
+  bf16x8 sb[QB][2];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      float p = __builtin_amdgcn_exp2f(fmaf(s[qb][r], c, nl2[qb]));
+      if constexpr (RAGGED) {  // keys past the clip must not contribute
+        const int key = (r >> 2) * 8 + G * 4 + (r & 3);
+        p = key < nvalid ? p : 0.0f;
+      }
+      s[qb][r] = p * (dp[qb][r] - dlt[qb]);
+    }
+    sb[qb][0] = to_bf16x8(s[qb], 0);
+    sb[qb][1] = to_bf16x8(s[qb], 8);
+  }
+  // dQ^T += K^T dS^T over the 16 keys of half hf.
+#pragma unroll
+  for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) dqa[qb][db] = mfma(kt[hf][db], sb[qb][hf], dqa[qb][db]);
+}
+
+template <int D, int QB>
+__global__ __launch_bounds__(kThreads, 2) void attn_bwd_dq_kernel(
+    const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
+    const bf16* __restrict__ dout, const float* __restrict__ lse2, const float* __restrict__ delta,
+    const Item* __restrict__ items, int H, int64_t T, float c, float scale, bf16* __restrict__ dq) {
+  constexpr int KK = D / 16;
+  constexpr int DB = D / 32;
+  constexpr int BN = 64;
+  __shared__ __attribute__((aligned(1024))) bf16 sK[2][BN * D];
+  __shared__ __attribute__((aligned(1024))) bf16 sV[2][BN * D];
+
+  const Item it = items[blockIdx.x];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int G = lane >> 5;
+  const int l32 = lane & 31;
+  const int L = it.len;
+  const int64_t rs = static_cast<int64_t>(H) * D;
+  const int64_t base = static_cast<int64_t>(it.row0) * rs + static_cast<int64_t>(it.head) * D;
+  const int64_t lbase = static_cast<int64_t>(it.head) * T + it.row0;
+  const bf16* kh = k + base;
+  const bf16* vh = v + base;
+  const int q_wave0 = it.tile0 + wave * QB * 32;
+  const bool wave_active = q_wave0 < L;
+
+  tile_dma<D, BN, kThreads>(sK[0], kh, rs, 0, L, tid);
+  tile_dma<D, BN, kThreads>(sV[0], vh, rs, 0, L, tid);
+
+  bf16x8 qop[QB][KK], gop[QB][KK];
+  float nl2[QB], dlt[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const int qi = q_wave0 + qb * 32 + l32;
+    const bool ok = qi < L;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      qop[qb][kk] = load8(q + base + qi * rs + kk * 16 + G * 8, ok);
+      gop[qb][kk] = load8(dout + base + qi * rs + kk * 16 + G * 8, ok);
+    }
+    nl2[qb] = ok ? -lse2[lbase + qi] : 0.0f;
+    dlt[qb] = ok ? delta[lbase + qi] : 0.0f;
+  }
+  f32x16 dqa[QB][DB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+    for (int db = 0; db < DB; ++db) dqa[qb][db] = zero16();
+
+  const int ntiles = (L + BN - 1) / BN;
+  const int nfull = L / BN;
+  const uint32_t oo = opnd_lane_off<D>(lane);
+  const uint32_t ro0 = rows_lane_off<D>(lane, 0), ro1 = rows_lane_off<D>(lane, 1);
+  wait_vmcnt0();
+  __syncthreads();
+  for (int tt = 0; tt < nfull; ++tt) {
+    const int b = tt & 1;
+    if (tt + 1 < ntiles) {
+      tile_dma<D, BN, kThreads>(sK[b ^ 1], kh, rs, (tt + 1) * BN, L, tid);
+      tile_dma<D, BN, kThreads>(sV[b ^ 1], vh, rs, (tt + 1) * BN, L, tid);
+    }
+    if (wave_active) {
+      const uint32_t tk = lds_addr(sK[b]);
+      const uint32_t kb0 = tk + oo, vb0 = lds_addr(sV[b]) + oo, k0 = tk + ro0, k1 = tk + ro1;
+      dq_step<D, QB, false>(kb0, vb0, k0, k1, 0, 32, c, qop, gop, nl2, dlt, dqa, lane);
+      dq_step<D, QB, false>(kb0, vb0, k0, k1, 32, 32, c, qop, gop, nl2, dlt, dqa, lane);
+    }
+    wait_vmcnt0();
+    __syncthreads();
+  }
+  if (nfull < ntiles && wave_active) {
+    const int b = nfull & 1;
+    const int rem = L - nfull * BN;
+    const uint32_t tk = lds_addr(sK[b]);
+    const uint32_t kb0 = tk + oo, vb0 = lds_addr(sV[b]) + oo, k0 = tk + ro0, k1 = tk + ro1;
+    if (rem >= 32) {
+      dq_step<D, QB, false>(kb0, vb0, k0, k1, 0, 32, c, qop, gop, nl2, dlt, dqa, lane);
+      if (rem > 32) dq_step<D, QB, true>(kb0, vb0, k0, k1, 32, rem - 32, c, qop, gop, nl2, dlt, dqa, lane);
+    } else {
+      dq_step<D, QB, true>(kb0, vb0, k0, k1, 0, rem, c, qop, gop, nl2, dlt, dqa, lane);
+    }
+  }
+
+  if (wave_active) {
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      const int qi = q_wave0 + qb * 32 + l32;
+      if (qi < L) {
+        bf16* row = dq + base + qi * rs;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            bf16x4 w;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) w[e] = static_cast<bf16>(dqa[qb][db][i * 4 + e] * scale);
+            *reinterpret_cast<bf16x4*>(row + db * 32 + i * 8 + G * 4) = w;
+          }
+        }
+      }
+    }
+  }
+}
+
+}  // namespace
+
+int dq_tile_rows(int) { return (kThreads / 64) * 32 * kDqQB; }
+
+hipError_t launch_bwd_dq(const AttnArgs& a, const Item* items, int n_items, hipStream_t stream) {
+  const float c = a.scale * kLog2e;
+  const dim3 grid(n_items), block(kThreads);
+  const auto* q = static_cast<const bf16*>(a.q);
+  const auto* k = static_cast<const bf16*>(a.k);
+  const auto* v = static_cast<const bf16*>(a.v);
+  const auto* g = static_cast<const bf16*>(a.dout);
+  auto* dq = static_cast<bf16*>(a.dq);
+  const float* lse2 = a.delta + a.total_tokens * a.heads;
+  if (a.head_dim == 128)
+    hipLaunchKernelGGL((attn_bwd_dq_kernel<128, kDqQB>), grid, block, 0, stream, q, k, v, g, lse2, a.delta,
+                       items, a.heads, a.total_tokens, c, a.scale, dq);
+  else
+    hipLaunchKernelGGL((attn_bwd_dq_kernel<64, kDqQB>), grid, block, 0, stream, q, k, v, g, lse2, a.delta,
+                       items, a.heads, a.total_tokens, c, a.scale, dq);
+  return hipGetLastError();
+}
+}  // namespace t2v

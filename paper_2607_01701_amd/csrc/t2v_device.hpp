@@ -88,16 +88,23 @@ T2V_DEV bf16x8 lds_read_rows_operand(const bf16* tile, int stride, int row0, int
 // ---------------------------------------------------------------- swizzled LDS tiles
 //
 // A tile of R rows x D bf16 is stored unpadded (row stride D) with its 16-byte chunks
-// permuted within each row: logical chunk c of row r sits in slot c ^ swz(r). swz maps
-// r % 8 to a permutation of 0..7 chosen so that both access patterns are free of bank
-// conflicts: eight consecutive rows at one chunk (the 16-byte operand reads) and four
-// consecutive rows x two adjacent chunks (the transposing 8-byte reads).
-T2V_DEV int swz(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
+// permuted within each row: logical chunk c of row r sits in slot c ^ swz<D>(r). gfx950's
+// LDS serves 256 bytes (64 banks of 4 bytes) per cycle, i.e. 16 lanes of a 16-byte read.
+// For D = 128 (256-byte rows) swz permutes r mod 16 onto 0..15 so that both access patterns
+// are free of bank conflicts: sixteen consecutive rows at one chunk (the 16-byte operand
+// reads) and four consecutive rows x two adjacent chunks per 16 lanes (the transposing 8-byte
+// reads); measured 186 and 93 bytes/clock/CU, against 100 and 92 for an 8-way permutation.
+// For D = 64 (128-byte rows, two rows per bank line) it permutes (r / 2) mod 8.
+template <int D>
+T2V_DEV int swz(int r) {
+  if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
+  return (r >> 1) & 7;
+}
 
 // Element offset of (row r, column col) in a swizzled tile; col % 8 is kept.
 template <int D>
 T2V_DEV int swz_off(int r, int col) {
-  return r * D + (((col >> 3) ^ swz(r)) << 3) + (col & 7);
+  return r * D + (((col >> 3) ^ swz<D>(r)) << 3) + (col & 7);
 }
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -120,7 +127,7 @@ T2V_DEV void tile_dma(bf16* tile, const bf16* g, int64_t rs, int row0, int L, in
 #pragma unroll
   for (int i = wave; i < NI; i += NW) {
     const int r = i * RPI + lane / CPR;
-    const int c = (lane % CPR) ^ swz(r);
+    const int c = (lane % CPR) ^ swz<D>(r);
     const int gr = min(row0 + r, L - 1);
     __builtin_amdgcn_global_load_lds(g + gr * rs + c * 8, (lds_void*)(tile + i * 512), 16, 0, 0);
   }
@@ -132,7 +139,7 @@ T2V_DEV void wait_vmcnt0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 // 16-byte operand read of logical chunk `chunk` of row r from a swizzled tile.
 template <int D>
 T2V_DEV bf16x8 swz_read8(const bf16* tile, int r, int chunk) {
-  return *reinterpret_cast<const bf16x8*>(tile + r * D + ((chunk ^ swz(r)) << 3));
+  return *reinterpret_cast<const bf16x8*>(tile + r * D + ((chunk ^ swz<D>(r)) << 3));
 }
 
 // As lds_read_rows_operand, for a swizzled tile with row stride D.
@@ -145,6 +152,58 @@ T2V_DEV bf16x8 swz_read_rows_operand(const bf16* tile, int row0, int col0, int l
   const int col = col0 + 16 * dhalf + 4 * (s & 3);
   bf16x4 lo = lds_read_tr4(tile + swz_off<D>(r, col));
   bf16x4 hi = lds_read_tr4(tile + swz_off<D>(r + 8, col));
+  bf16x8 out;
+  out[0] = lo[0]; out[1] = lo[1]; out[2] = lo[2]; out[3] = lo[3];
+  out[4] = hi[0]; out[5] = hi[1]; out[6] = hi[2]; out[7] = hi[3];
+  return out;
+}
+
+// ---------------------------------------------------------------- LDS addressing
+//
+// Operand reads address swizzled tiles with 32-bit LDS byte addresses. Two identities
+// (checked exhaustively for every lane on the host, see tests/test_lds_layout.py) make each read one
+// base register plus one XOR: for the 16-byte operand of row (32j + lane % 32), chunk 2 kk + G,
+//   off(kk) = off(0) ^ (kk << 5) ;
+// for the transposing read of rows (16i + 4G + s/4 + 8h), column 32 db + 16 dh + 4 (s % 4),
+//   off(db) = off(0) ^ (db << 6) ;
+// and rows that differ by a multiple of 16 differ by a constant (folded into the instruction's
+// immediate offset). Tile bases are 1 KB aligned, so base + (o ^ x) == (base + o) ^ x.
+typedef __attribute__((address_space(3))) char lds_char;
+typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+T2V_DEV uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const lds_char*)p));
+}
+T2V_DEV bf16x8 lds_ld8(uint32_t a) { return *(const lds_bf16x8*)(a); }
+T2V_DEV bf16x4 lds_ld_tr4(uint32_t a) {
+  return __builtin_bit_cast(bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(a)));
+}
+
+// Byte offsets of this lane's reads within a swizzled tile (row base 0, kk = 0, db = 0).
+template <int D>
+T2V_DEV uint32_t opnd_lane_off(int lane) {
+  return 2u * static_cast<uint32_t>(swz_off<D>(lane & 31, 8 * (lane >> 5)));
+}
+template <int D>
+T2V_DEV uint32_t rows_lane_off(int lane, int h) {
+  const int G = lane >> 5, s = lane & 15, dh = (lane >> 4) & 1;
+  return 2u * static_cast<uint32_t>(swz_off<D>(4 * G + (s >> 2) + 8 * h, 16 * dh + 4 * (s & 3)));
+}
+
+// 16-byte operand: row row0 + lane % 32 (row0 a multiple of 32), chunk 2 kk + G.
+template <int D>
+T2V_DEV bf16x8 read_opnd(uint32_t base, int row0, int kk) {
+  return lds_ld8((base ^ static_cast<uint32_t>(kk << 5)) + static_cast<uint32_t>(row0 * 2 * D));
+}
+
+// Operand whose contraction index runs down the rows (see lds_read_rows_operand), rows
+// row0 .. row0 + 15 (row0 a multiple of 16), columns 32 db .. 32 db + 31.
+template <int D>
+T2V_DEV bf16x8 read_rows_opnd(uint32_t base0, uint32_t base1, int row0, int db) {
+  const uint32_t x = static_cast<uint32_t>(db << 6), ro = static_cast<uint32_t>(row0 * 2 * D);
+  const bf16x4 lo = lds_ld_tr4((base0 ^ x) + ro);
+  const bf16x4 hi = lds_ld_tr4((base1 ^ x) + ro);
   bf16x8 out;
   out[0] = lo[0]; out[1] = lo[1]; out[2] = lo[2]; out[3] = lo[3];
   out[4] = hi[0]; out[5] = hi[1]; out[6] = hi[2]; out[7] = hi[3];

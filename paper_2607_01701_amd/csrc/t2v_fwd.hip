@@ -1,0 +1,268 @@
+// gfx950 kernels for packed variable-length bidirectional attention.
+//
+// One workgroup = 4 waves = 256 threads, one work item (a tile of one clip and one
+// head, from the host scheduler). All products use v_mfma_f32_32x32x16_bf16 with fp32
+// accumulation; K/V (forward, dQ) or Q/dO (dK/dV) tiles are staged through LDS with a
+// two-buffer pipeline: the global loads for tile t+1 are issued before the MFMA work on
+// tile t and land in the other LDS buffer after it, one barrier per tile.
+//
+// Forward (paper Section III, Observation 2: full self-attention over each clip):
+// every lane owns one query row of a 32-query block, because scores are computed
+// transposed (S^T = K Q^T), so row max/sum need one swap with the other wave half.
+// The softmax is online over 32-key steps with a lazily moved reference maximum:
+// the reference m only moves when a step's maximum exceeds it by more than kTau (in
+// log2 units), which keeps every exp2 argument <= kTau and lets most steps skip the
+// rescale of the output accumulator. The final O / l and lse = ln2 (m + log2 l) are
+// exact for any reference m, so the result is the plain softmax up to rounding.
+//
+// Backward (Fig. 1 caption: the DiT backward pass): Delta = rowsum(dO * O), then a
+// dK/dV kernel (a workgroup owns 128 keys, loops over the clip's queries) and a dQ
+// kernel (a workgroup owns a query tile, loops over the clip's keys). P is recomputed
+// from the stored lse; nothing is accumulated across workgroups, so there are no
+// atomics and results are bitwise reproducible.
+#include "t2v_kernel_common.hpp"
+
+namespace t2v {
+
+using namespace kern;
+
+namespace {
+
+constexpr int kFwdQB = 1;  // 32-query blocks per wave
+
+// ------------------------------------------------------------------------------ forward
+
+// Sum / max of the 16 values of an accumulator as a balanced tree (short dependency chains).
+T2V_DEV float tree_sum16(const f32x16& x) {
+  float a[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) a[i] = x[i] + x[i + 8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) a[i] += a[i + 4];
+  return (a[0] + a[2]) + (a[1] + a[3]);
+}
+
+template <bool NEG>
+T2V_DEV float tree_ext16(const f32x16& x) {
+  float a[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) a[i] = NEG ? fminf(x[i], x[i + 8]) : fmaxf(x[i], x[i + 8]);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) a[i] = NEG ? fminf(a[i], a[i + 4]) : fmaxf(a[i], a[i + 4]);
+  const float b0 = NEG ? fminf(a[0], a[2]) : fmaxf(a[0], a[2]);
+  const float b1 = NEG ? fminf(a[1], a[3]) : fmaxf(a[1], a[3]);
+  return NEG ? fminf(b0, b1) : fmaxf(b0, b1);
+}
+
+// One 32-key step of the forward pass for QB query blocks of this wave.
+// sK/sV: the LDS stage; kb: first key of the step within the stage; nvalid: keys of the
+// step inside the clip (only read when RAGGED, where it is 1..31).
+template <int D, int QB, bool NEG, bool RAGGED>
+T2V_DEV void fwd_step(uint32_t kbase, uint32_t vbase0, uint32_t vbase1, int kb, int nvalid, float c,
+                      const bf16x8 (&qop)[QB][D / 16], f32x16 (&o)[QB][D / 32], float (&m_run)[QB],
+                      float (&l_run)[QB], int lane) {
+  constexpr int KK = D / 16;
+  constexpr int DB = D / 32;
+  const int G = lane >> 5;
+  const int l32 = lane & 31;
+  // S^T (32 keys x 32 queries per block): lane = query, register r = key 8 (r/4) + 4 G + r % 4.
+  bf16x8 ka[KK];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) ka[kk] = read_opnd<D>(kbase, kb, kk);
+  f32x16 s[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) s[qb] = zero16();
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) {
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) s[qb] = mfma(ka[kk], qop[qb][kk], s[qb]);
+  }
+  // V operands are read now so their LDS latency overlaps the softmax arithmetic.
+  bf16x8 va[2][DB];
+#pragma unroll
+  for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+    for (int db = 0; db < DB; ++db) va[hf][db] = read_rows_opnd<D>(vbase0, vbase1, kb + hf * 16, db);
+  bf16x8 pb[QB][2];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    if constexpr (RAGGED) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = (r >> 2) * 8 + G * 4 + (r & 3);
+        if (key >= nvalid) s[qb][r] = NEG ? kInf : -kInf;
+      }
+    }
+    float mx = tree_ext16<NEG>(s[qb]);
+    mx = NEG ? half_min(mx) : half_max(mx);
+    const float mblk = mx * c;  // largest scaled score of this step
+    if (__any(mblk > m_run[qb] + kTau)) {
+      const float mn = fmaxf(m_run[qb], mblk);
+      const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - mn);
+      l_run[qb] *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) o[qb][db] *= alpha;
+      m_run[qb] = mn;
+    }
+    const float nm = -m_run[qb];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      float p = __builtin_amdgcn_exp2f(fmaf(s[qb][r], c, nm));
+      if constexpr (RAGGED) {
+        const int key = (r >> 2) * 8 + G * 4 + (r & 3);
+        p = key < nvalid ? p : 0.0f;  // also covers scale = 0, where c * -inf is NaN
+      }
+      s[qb][r] = p;
+    }
+    l_run[qb] += tree_sum16(s[qb]);
+    pb[qb][0] = to_bf16x8(s[qb], 0);
+    pb[qb][1] = to_bf16x8(s[qb], 8);
+  }
+  // O^T += V^T P^T: the key of P element t (from register 8 hf + t) is
+  // kb + 16 hf + 8 (t / 4) + 4 G + t % 4, which is how the V operand is read.
+#pragma unroll
+  for (int hf = 0; hf < 2; ++hf) {
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) o[qb][db] = mfma(va[hf][db], pb[qb][hf], o[qb][db]);
+    }
+  }
+}
+
+template <int D, int QB, bool NEG>
+__global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
+    const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
+    const Item* __restrict__ items, int H, int64_t T, float c, bf16* __restrict__ out,
+    float* __restrict__ lse) {
+  constexpr int KK = D / 16;  // k-steps of the head-dim contraction
+  constexpr int DB = D / 32;  // 32-wide head-dim blocks of the output
+  constexpr int BN = 64;      // keys per LDS stage
+  __shared__ __attribute__((aligned(1024))) bf16 sK[2][BN * D];
+  __shared__ __attribute__((aligned(1024))) bf16 sV[2][BN * D];
+
+  const Item it = items[blockIdx.x];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int G = lane >> 5;
+  const int l32 = lane & 31;
+  const int L = it.len;
+  const int64_t rs = static_cast<int64_t>(H) * D;  // elements between consecutive tokens
+  const int64_t base = static_cast<int64_t>(it.row0) * rs + static_cast<int64_t>(it.head) * D;
+  const bf16* kh = k + base;
+  const bf16* vh = v + base;
+  const int q_wave0 = it.tile0 + wave * QB * 32;
+  const bool wave_active = q_wave0 < L;
+
+  tile_dma<D, BN, kThreads>(sK[0], kh, rs, 0, L, tid);
+  tile_dma<D, BN, kThreads>(sV[0], vh, rs, 0, L, tid);
+
+  bf16x8 qop[QB][KK];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const int qi = q_wave0 + qb * 32 + l32;
+    const bool ok = qi < L;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) qop[qb][kk] = load8(q + base + qi * rs + kk * 16 + G * 8, ok);
+  }
+
+  f32x16 o[QB][DB];
+  float m_run[QB], l_run[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    m_run[qb] = -kInf;
+    l_run[qb] = 0.0f;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) o[qb][db] = zero16();
+  }
+
+  const int ntiles = (L + BN - 1) / BN;
+  const int nfull = L / BN;  // tiles with BN keys of the clip
+  const uint32_t ko = opnd_lane_off<D>(lane);
+  const uint32_t vo0 = rows_lane_off<D>(lane, 0), vo1 = rows_lane_off<D>(lane, 1);
+  wait_vmcnt0();
+  __syncthreads();
+  for (int tt = 0; tt < nfull; ++tt) {
+    const int b = tt & 1;
+    if (tt + 1 < ntiles) {
+      tile_dma<D, BN, kThreads>(sK[b ^ 1], kh, rs, (tt + 1) * BN, L, tid);
+      tile_dma<D, BN, kThreads>(sV[b ^ 1], vh, rs, (tt + 1) * BN, L, tid);
+    }
+    if (wave_active) {
+      const uint32_t kbase = lds_addr(sK[b]) + ko;
+      const uint32_t vb0 = lds_addr(sV[b]) + vo0, vb1 = lds_addr(sV[b]) + vo1;
+      fwd_step<D, QB, NEG, false>(kbase, vb0, vb1, 0, 32, c, qop, o, m_run, l_run, lane);
+      fwd_step<D, QB, NEG, false>(kbase, vb0, vb1, 32, 32, c, qop, o, m_run, l_run, lane);
+    }
+    wait_vmcnt0();
+    __syncthreads();
+  }
+  if (nfull < ntiles && wave_active) {  // last tile, 1 .. BN-1 keys
+    const int b = nfull & 1;
+    const int rem = L - nfull * BN;
+    const uint32_t kbase = lds_addr(sK[b]) + ko;
+    const uint32_t vb0 = lds_addr(sV[b]) + vo0, vb1 = lds_addr(sV[b]) + vo1;
+    if (rem >= 32) {
+      fwd_step<D, QB, NEG, false>(kbase, vb0, vb1, 0, 32, c, qop, o, m_run, l_run, lane);
+      if (rem > 32) fwd_step<D, QB, NEG, true>(kbase, vb0, vb1, 32, rem - 32, c, qop, o, m_run, l_run, lane);
+    } else {
+      fwd_step<D, QB, NEG, true>(kbase, vb0, vb1, 0, rem, c, qop, o, m_run, l_run, lane);
+    }
+  }
+
+  if (wave_active) {
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      const int qi = q_wave0 + qb * 32 + l32;
+      const float lt = half_sum(l_run[qb]);
+      const float inv = 1.0f / lt;
+      if (qi < L) {
+        bf16* orow = out + base + qi * rs;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            bf16x4 w;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) w[e] = static_cast<bf16>(o[qb][db][i * 4 + e] * inv);
+            *reinterpret_cast<bf16x4*>(orow + db * 32 + i * 8 + G * 4) = w;
+          }
+        }
+        if (G == 0) lse[static_cast<int64_t>(it.head) * T + it.row0 + qi] = (m_run[qb] + __builtin_amdgcn_logf(lt)) * kLn2;
+      }
+    }
+  }
+}
+
+}  // namespace
+
+int fwd_tile_rows(int) { return (kThreads / 64) * 32 * kFwdQB; }
+
+hipError_t launch_fwd(const AttnArgs& a, void* out, float* lse, const Item* items, int n_items,
+                      hipStream_t stream) {
+  const float c = a.scale * kLog2e;
+  const auto* q = static_cast<const bf16*>(a.q);
+  const auto* k = static_cast<const bf16*>(a.k);
+  const auto* v = static_cast<const bf16*>(a.v);
+  auto* o = static_cast<bf16*>(out);
+  const dim3 grid(n_items), block(kThreads);
+  const bool neg = a.scale < 0.0f;
+  if (a.head_dim == 128) {
+    if (neg)
+      hipLaunchKernelGGL((attn_fwd_kernel<128, kFwdQB, true>), grid, block, 0, stream, q, k, v, items, a.heads,
+                         a.total_tokens, c, o, lse);
+    else
+      hipLaunchKernelGGL((attn_fwd_kernel<128, kFwdQB, false>), grid, block, 0, stream, q, k, v, items, a.heads,
+                         a.total_tokens, c, o, lse);
+  } else {
+    if (neg)
+      hipLaunchKernelGGL((attn_fwd_kernel<64, kFwdQB, true>), grid, block, 0, stream, q, k, v, items, a.heads,
+                         a.total_tokens, c, o, lse);
+    else
+      hipLaunchKernelGGL((attn_fwd_kernel<64, kFwdQB, false>), grid, block, 0, stream, q, k, v, items, a.heads,
+                         a.total_tokens, c, o, lse);
+  }
+  return hipGetLastError();
+}
+}  // namespace t2v
