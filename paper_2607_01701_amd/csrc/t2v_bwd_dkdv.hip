@@ -8,6 +8,8 @@ using namespace kern;
 
 namespace {
 
+constexpr int kDkdvBM = 64;  // queries per LDS stage (a multiple of 32)
+
 // Asynchronous copy of 64 consecutive floats (rows row0 .. row0 + 63, clamped to L - 1)
 // into LDS, by one wave.
 T2V_DEV void rows64_dma(float* lds, const float* g, int row0, int L, int lane) {
@@ -24,6 +26,8 @@ T2V_DEV void dkdv_step(uint32_t qbase, uint32_t gbase, uint32_t qr0, uint32_t qr
                        const float* sL2, const float* sDl, int qs, int nvalid,
                        float c, const bf16x8 (&kop)[D / 16], const bf16x8 (&vop)[D / 16], f32x16 (&dka)[D / 32],
                        f32x16 (&dva)[D / 32], int lane) {
+  // Let the scheduler interleave this step's LDS reads with its MFMAs (measured: +2 to +4%).
+  __builtin_amdgcn_iglp_opt(0);
   constexpr int KK = D / 16;
   constexpr int DB = D / 32;
   const int G = lane >> 5;
@@ -82,7 +86,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
     bf16* __restrict__ dv) {
   constexpr int KK = D / 16;
   constexpr int DB = D / 32;
-  constexpr int BM = 64;  // queries per LDS stage
+  constexpr int BM = kDkdvBM;  // queries per LDS stage
   __shared__ __attribute__((aligned(1024))) bf16 sQ[2][BM * D];
   __shared__ __attribute__((aligned(1024))) bf16 sG[2][BM * D];  // dO
   __shared__ __attribute__((aligned(16))) float sL[2][BM];       // lse * log2(e)
@@ -108,8 +112,14 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
   auto stage = [&](int b, int i0) {
     tile_dma<D, BM, kThreads>(sQ[b], qh, rs, i0, L, tid);
     tile_dma<D, BM, kThreads>(sG[b], gh, rs, i0, L, tid);
-    if (wave == 0) rows64_dma(sL[b], l2h, i0, L, lane);
-    if (wave == 1) rows64_dma(sD[b], dlh, i0, L, lane);
+    // BM floats of lse2 and of Delta, 64 per wave instruction (lanes past BM idle).
+#pragma unroll
+    for (int j = wave; j < 2 * ((BM + 63) / 64); j += kThreads / 64) {
+      const int half = (BM + 63) / 64;
+      const int part = j < half ? j : j - half;
+      if (part * 64 + lane < BM)
+        rows64_dma((j < half ? sL[b] : sD[b]) + part * 64, j < half ? l2h : dlh, i0 + part * 64, L, lane);
+    }
   };
   stage(0, 0);
 
@@ -144,8 +154,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
       const uint32_t tq = lds_addr(sQ[b]), tg = lds_addr(sG[b]);
       const uint32_t qb = tq + oo, gb = tg + oo;
       const uint32_t q0 = tq + ro0, q1 = tq + ro1, g0 = tg + ro0, g1 = tg + ro1;
-      dkdv_step<D, false>(qb, gb, q0, q1, g0, g1, sL[b], sD[b], 0, 32, c, kop, vop, dka, dva, lane);
-      dkdv_step<D, false>(qb, gb, q0, q1, g0, g1, sL[b], sD[b], 32, 32, c, kop, vop, dka, dva, lane);
+#pragma unroll
+      for (int qs = 0; qs < BM; qs += 32)
+        dkdv_step<D, false>(qb, gb, q0, q1, g0, g1, sL[b], sD[b], qs, 32, c, kop, vop, dka, dva, lane);
     }
     wait_vmcnt0();
     __syncthreads();
@@ -156,12 +167,12 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
     const uint32_t tq = lds_addr(sQ[b]), tg = lds_addr(sG[b]);
     const uint32_t qb = tq + oo, gb = tg + oo;
     const uint32_t q0 = tq + ro0, q1 = tq + ro1, g0 = tg + ro0, g1 = tg + ro1;
-    if (rem >= 32) {
-      dkdv_step<D, false>(qb, gb, q0, q1, g0, g1, sL[b], sD[b], 0, 32, c, kop, vop, dka, dva, lane);
-      if (rem > 32)
-        dkdv_step<D, true>(qb, gb, q0, q1, g0, g1, sL[b], sD[b], 32, rem - 32, c, kop, vop, dka, dva, lane);
-    } else {
-      dkdv_step<D, true>(qb, gb, q0, q1, g0, g1, sL[b], sD[b], 0, rem, c, kop, vop, dka, dva, lane);
+#pragma unroll
+    for (int qs = 0; qs < BM; qs += 32) {
+      if (rem >= qs + 32)
+        dkdv_step<D, false>(qb, gb, q0, q1, g0, g1, sL[b], sD[b], qs, 32, c, kop, vop, dka, dva, lane);
+      else if (rem > qs)
+        dkdv_step<D, true>(qb, gb, q0, q1, g0, g1, sL[b], sD[b], qs, rem - qs, c, kop, vop, dka, dva, lane);
     }
   }
 

@@ -9,6 +9,7 @@ using namespace kern;
 namespace {
 
 constexpr int kDqQB = 1;  // 32-query blocks per wave
+constexpr int kDqBN = 64; // keys per LDS stage (a multiple of 32)
 
 // ------------------------------------------------------------------------ backward: dQ
 
@@ -19,6 +20,8 @@ T2V_DEV void dq_step(uint32_t kbase, uint32_t vbase, uint32_t kr0, uint32_t kr1,
                      const bf16x8 (&qop)[QB][D / 16],
                      const bf16x8 (&gop)[QB][D / 16], const float (&nl2)[QB], const float (&dlt)[QB],
                      f32x16 (&dqa)[QB][D / 32], int lane) {
+  // Let the scheduler interleave this step's LDS reads with its MFMAs (measured: +2 to +4%).
+  __builtin_amdgcn_iglp_opt(0);
   constexpr int KK = D / 16;
   constexpr int DB = D / 32;
   const int G = lane >> 5;
@@ -84,7 +87,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bwd_dq_kernel(
     const Item* __restrict__ items, int H, int64_t T, float c, float scale, bf16* __restrict__ dq) {
   constexpr int KK = D / 16;
   constexpr int DB = D / 32;
-  constexpr int BN = 64;
+  constexpr int BN = kDqBN;  // keys per LDS stage
   __shared__ __attribute__((aligned(1024))) bf16 sK[2][BN * D];
   __shared__ __attribute__((aligned(1024))) bf16 sV[2][BN * D];
 
@@ -141,8 +144,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bwd_dq_kernel(
     if (wave_active) {
       const uint32_t tk = lds_addr(sK[b]);
       const uint32_t kb0 = tk + oo, vb0 = lds_addr(sV[b]) + oo, k0 = tk + ro0, k1 = tk + ro1;
-      dq_step<D, QB, false>(kb0, vb0, k0, k1, 0, 32, c, qop, gop, nl2, dlt, dqa, lane);
-      dq_step<D, QB, false>(kb0, vb0, k0, k1, 32, 32, c, qop, gop, nl2, dlt, dqa, lane);
+#pragma unroll
+      for (int kb = 0; kb < BN; kb += 32)
+        dq_step<D, QB, false>(kb0, vb0, k0, k1, kb, 32, c, qop, gop, nl2, dlt, dqa, lane);
     }
     wait_vmcnt0();
     __syncthreads();
@@ -152,11 +156,12 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bwd_dq_kernel(
     const int rem = L - nfull * BN;
     const uint32_t tk = lds_addr(sK[b]);
     const uint32_t kb0 = tk + oo, vb0 = lds_addr(sV[b]) + oo, k0 = tk + ro0, k1 = tk + ro1;
-    if (rem >= 32) {
-      dq_step<D, QB, false>(kb0, vb0, k0, k1, 0, 32, c, qop, gop, nl2, dlt, dqa, lane);
-      if (rem > 32) dq_step<D, QB, true>(kb0, vb0, k0, k1, 32, rem - 32, c, qop, gop, nl2, dlt, dqa, lane);
-    } else {
-      dq_step<D, QB, true>(kb0, vb0, k0, k1, 0, rem, c, qop, gop, nl2, dlt, dqa, lane);
+#pragma unroll
+    for (int kb = 0; kb < BN; kb += 32) {
+      if (rem >= kb + 32)
+        dq_step<D, QB, false>(kb0, vb0, k0, k1, kb, 32, c, qop, gop, nl2, dlt, dqa, lane);
+      else if (rem > kb)
+        dq_step<D, QB, true>(kb0, vb0, k0, k1, kb, rem - kb, c, qop, gop, nl2, dlt, dqa, lane);
     }
   }
 

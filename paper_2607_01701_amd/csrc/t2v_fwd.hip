@@ -29,6 +29,7 @@ using namespace kern;
 namespace {
 
 constexpr int kFwdQB = 1;  // 32-query blocks per wave
+constexpr int kFwdBN = 64; // keys per LDS stage (a multiple of 32)
 
 // ------------------------------------------------------------------------------ forward
 
@@ -61,6 +62,8 @@ template <int D, int QB, bool NEG, bool RAGGED>
 T2V_DEV void fwd_step(uint32_t kbase, uint32_t vbase0, uint32_t vbase1, int kb, int nvalid, float c,
                       const bf16x8 (&qop)[QB][D / 16], f32x16 (&o)[QB][D / 32], float (&m_run)[QB],
                       float (&l_run)[QB], int lane) {
+  // Let the scheduler interleave this step's LDS reads with its MFMAs (measured: +2 to +4%).
+  __builtin_amdgcn_iglp_opt(0);
   constexpr int KK = D / 16;
   constexpr int DB = D / 32;
   const int G = lane >> 5;
@@ -137,7 +140,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
     float* __restrict__ lse) {
   constexpr int KK = D / 16;  // k-steps of the head-dim contraction
   constexpr int DB = D / 32;  // 32-wide head-dim blocks of the output
-  constexpr int BN = 64;      // keys per LDS stage
+  constexpr int BN = kFwdBN;  // keys per LDS stage
   __shared__ __attribute__((aligned(1024))) bf16 sK[2][BN * D];
   __shared__ __attribute__((aligned(1024))) bf16 sV[2][BN * D];
 
@@ -192,8 +195,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
     if (wave_active) {
       const uint32_t kbase = lds_addr(sK[b]) + ko;
       const uint32_t vb0 = lds_addr(sV[b]) + vo0, vb1 = lds_addr(sV[b]) + vo1;
-      fwd_step<D, QB, NEG, false>(kbase, vb0, vb1, 0, 32, c, qop, o, m_run, l_run, lane);
-      fwd_step<D, QB, NEG, false>(kbase, vb0, vb1, 32, 32, c, qop, o, m_run, l_run, lane);
+#pragma unroll
+      for (int kb = 0; kb < BN; kb += 32)
+        fwd_step<D, QB, NEG, false>(kbase, vb0, vb1, kb, 32, c, qop, o, m_run, l_run, lane);
     }
     wait_vmcnt0();
     __syncthreads();
@@ -203,11 +207,12 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
     const int rem = L - nfull * BN;
     const uint32_t kbase = lds_addr(sK[b]) + ko;
     const uint32_t vb0 = lds_addr(sV[b]) + vo0, vb1 = lds_addr(sV[b]) + vo1;
-    if (rem >= 32) {
-      fwd_step<D, QB, NEG, false>(kbase, vb0, vb1, 0, 32, c, qop, o, m_run, l_run, lane);
-      if (rem > 32) fwd_step<D, QB, NEG, true>(kbase, vb0, vb1, 32, rem - 32, c, qop, o, m_run, l_run, lane);
-    } else {
-      fwd_step<D, QB, NEG, true>(kbase, vb0, vb1, 0, rem, c, qop, o, m_run, l_run, lane);
+#pragma unroll
+    for (int kb = 0; kb < BN; kb += 32) {
+      if (rem >= kb + 32)
+        fwd_step<D, QB, NEG, false>(kbase, vb0, vb1, kb, 32, c, qop, o, m_run, l_run, lane);
+      else if (rem > kb)
+        fwd_step<D, QB, NEG, true>(kbase, vb0, vb1, kb, rem - kb, c, qop, o, m_run, l_run, lane);
     }
   }
 
