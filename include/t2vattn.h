@@ -109,7 +109,8 @@ int t2v_build_worklist(const int32_t* cu_seqlens, int nseq, int heads, int block
 
 /* Host-only: the predicted makespan of a work list on `slots` identical workers, in units
  * of (rows x keys) tile cost, when items are taken in list order by the next free worker
- * (greedy list scheduling), plus the lower bound max(total / slots, largest item). */
+ * (greedy list scheduling), plus the lower bound max(total / slots, largest item).
+ * `items` holds n_items items of 4 int32 as returned by t2v_build_worklist. */
 int t2v_plan_makespan(const int32_t* items, int n_items, int block, int slots,
                       double* makespan_out, double* lower_bound_out);
 

@@ -8,41 +8,47 @@ using namespace kern;
 
 namespace {
 
-constexpr int kDkdvBM = 64;  // queries per LDS stage (a multiple of 32)
+constexpr int kDkdvBM = 64;     // queries per LDS stage (a multiple of 32)
+constexpr int kDkdvStages = 4;  // LDS stages: up to 3 tiles of Q / dO in flight during one tile's work
 
-// Asynchronous copy of 64 consecutive floats (rows row0 .. row0 + 63, clamped to L - 1)
-// into LDS, by one wave.
+// Asynchronous copy of consecutive floats into LDS, one per active lane of the calling
+// wave (lane i copies row row0 + i, clamped to L - 1, to lds[i]).
 T2V_DEV void rows64_dma(float* lds, const float* g, int row0, int L, int lane) {
   const int r = min(row0 + lane, L - 1);
-  __builtin_amdgcn_global_load_lds(g + r, (lds_void*)lds, 4, 0, 0);
+  dma_lds4(g + r, static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void*)lds)));
 }
 
 // ------------------------------------------------------------------- backward: dK, dV
 
-// One 32-query step for this wave's 32 keys. RAGGED: only the first nvalid queries of
-// the step are inside the clip (their P is forced to zero).
-template <int D, bool RAGGED>
-T2V_DEV void dkdv_step(uint32_t qbase, uint32_t gbase, uint32_t qr0, uint32_t qr1, uint32_t gr0, uint32_t gr1,
-                       const float* sL2, const float* sDl, int qs, int nvalid,
-                       float c, const bf16x8 (&kop)[D / 16], const bf16x8 (&vop)[D / 16], f32x16 (&dka)[D / 32],
-                       f32x16 (&dva)[D / 32], int lane) {
-  // Let the scheduler interleave this step's LDS reads with its MFMAs (measured: +2 to +4%).
-  __builtin_amdgcn_iglp_opt(0);
-  constexpr int KK = D / 16;
-  constexpr int DB = D / 32;
+// Score operands of one 32-query step: rows qs .. qs + 31 of the Q and dO tiles.
+template <int D>
+T2V_DEV void dkdv_read_scores(uint32_t qbase, uint32_t gbase, int qs, bf16x8 (&aq)[D / 16], bf16x8 (&ag)[D / 16]) {
+#pragma unroll
+  for (int kk = 0; kk < D / 16; ++kk) aq[kk] = read_opnd<D>(qbase, qs, kk);
+#pragma unroll
+  for (int kk = 0; kk < D / 16; ++kk) ag[kk] = read_opnd<D>(gbase, qs, kk);
+}
+
+// S and dP of one 32-query step for this wave's 32 keys (32 queries x 32 keys): lane =
+// key, register r = query qs + 8 (r/4) + 4 G + r % 4.
+template <int D>
+T2V_DEV void dkdv_scores_mfma(const bf16x8 (&aq)[D / 16], const bf16x8 (&ag)[D / 16], const bf16x8 (&kop)[D / 16],
+                              const bf16x8 (&vop)[D / 16], f32x16& s, f32x16& dp) {
+  s = zero16();
+  dp = zero16();
+#pragma unroll
+  for (int kk = 0; kk < D / 16; ++kk) s = mfma(aq[kk], kop[kk], s);
+#pragma unroll
+  for (int kk = 0; kk < D / 16; ++kk) dp = mfma(ag[kk], vop[kk], dp);
+}
+
+// P = exp2(c S - lse2) and dS = P (dP - Delta) of one step, in bf16 by 16-query half.
+// RAGGED: only the first nvalid queries of the step are inside the clip (their P is
+// forced to zero).
+template <bool RAGGED>
+T2V_DEV void dkdv_softmax(f32x16 s, f32x16 dp, const float* sL2, const float* sDl, int qs, int nvalid, float c,
+                          bf16x8 (&pb)[2], bf16x8 (&sb)[2], int lane) {
   const int G = lane >> 5;
-  const int l32 = lane & 31;
-  // S and dP (32 queries x 32 keys): lane = key, register r = query qs + 8 (r/4) + 4 G + r % 4.
-  bf16x8 aq[KK], ag[KK];
-#pragma unroll
-  for (int kk = 0; kk < KK; ++kk) aq[kk] = read_opnd<D>(qbase, qs, kk);
-#pragma unroll
-  for (int kk = 0; kk < KK; ++kk) ag[kk] = read_opnd<D>(gbase, qs, kk);
-  f32x16 s = zero16(), dp = zero16();
-#pragma unroll
-  for (int kk = 0; kk < KK; ++kk) s = mfma(aq[kk], kop[kk], s);
-#pragma unroll
-  for (int kk = 0; kk < KK; ++kk) dp = mfma(ag[kk], vop[kk], dp);
   f32x4 lv[4], dl[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -59,9 +65,17 @@ T2V_DEV void dkdv_step(uint32_t qbase, uint32_t gbase, uint32_t qr0, uint32_t qr
     s[r] = p;
     dp[r] = p * (dp[r] - dl[r >> 2][r & 3]);
   }
-  const bf16x8 pb[2] = {to_bf16x8(s, 0), to_bf16x8(s, 8)};
-  const bf16x8 sb[2] = {to_bf16x8(dp, 0), to_bf16x8(dp, 8)};
-  // dV += P^T dO and dK += dS^T Q, contracting over the 16 queries of half hf.
+  pb[0] = to_bf16x8(s, 0);
+  pb[1] = to_bf16x8(s, 8);
+  sb[0] = to_bf16x8(dp, 0);
+  sb[1] = to_bf16x8(dp, 8);
+}
+
+// dV += P^T dO and dK += dS^T Q for one step, contracting over the 16 queries of each half.
+template <int D>
+T2V_DEV void dkdv_grad_mfma(const bf16x8 (&pb)[2], const bf16x8 (&sb)[2], uint32_t qr0, uint32_t qr1, uint32_t gr0,
+                            uint32_t gr1, int qs, f32x16 (&dka)[D / 32], f32x16 (&dva)[D / 32]) {
+  constexpr int DB = D / 32;
 #pragma unroll
   for (int hf = 0; hf < 2; ++hf) {
     bf16x8 bg[DB], bq[DB];
@@ -78,6 +92,22 @@ T2V_DEV void dkdv_step(uint32_t qbase, uint32_t gbase, uint32_t qr0, uint32_t qr
   }
 }
 
+// One whole step (used for the ragged last tile).
+template <int D, bool RAGGED>
+T2V_DEV void dkdv_step(uint32_t qbase, uint32_t gbase, uint32_t qr0, uint32_t qr1, uint32_t gr0, uint32_t gr1,
+                       const float* sL2, const float* sDl, int qs, int nvalid,
+                       float c, const bf16x8 (&kop)[D / 16], const bf16x8 (&vop)[D / 16], f32x16 (&dka)[D / 32],
+                       f32x16 (&dva)[D / 32], int lane) {
+  // Let the scheduler interleave this step's LDS reads with its MFMAs (measured: +2 to +4%).
+  __builtin_amdgcn_iglp_opt(0);
+  bf16x8 aq[D / 16], ag[D / 16], pb[2], sb[2];
+  f32x16 s, dp;
+  dkdv_read_scores<D>(qbase, gbase, qs, aq, ag);
+  dkdv_scores_mfma<D>(aq, ag, kop, vop, s, dp);
+  dkdv_softmax<RAGGED>(s, dp, sL2, sDl, qs, nvalid, c, pb, sb, lane);
+  dkdv_grad_mfma<D>(pb, sb, qr0, qr1, gr0, gr1, qs, dka, dva);
+}
+
 template <int D>
 __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
@@ -86,11 +116,17 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
     bf16* __restrict__ dv) {
   constexpr int KK = D / 16;
   constexpr int DB = D / 32;
-  constexpr int BM = kDkdvBM;  // queries per LDS stage
-  __shared__ __attribute__((aligned(1024))) bf16 sQ[2][BM * D];
-  __shared__ __attribute__((aligned(1024))) bf16 sG[2][BM * D];  // dO
-  __shared__ __attribute__((aligned(16))) float sL[2][BM];       // lse * log2(e)
-  __shared__ __attribute__((aligned(16))) float sD[2][BM];       // Delta
+  constexpr int BM = kDkdvBM;      // queries per LDS stage
+  constexpr int NS = kDkdvStages;  // LDS stages in flight
+  constexpr int NW = kThreads / 64;
+  // DMA instructions per wave and stage: the Q and dO tiles, plus one 32-float piece of
+  // lse * log2(e) or Delta.
+  constexpr int kOps = 2 * (BM * D / 512) / NW + 1;
+  static_assert(2 * BM == 32 * NW, "each wave stages one 32-float piece of lse2 / Delta");
+  __shared__ __attribute__((aligned(1024))) bf16 sQ[NS][BM * D];
+  __shared__ __attribute__((aligned(1024))) bf16 sG[NS][BM * D];  // dO
+  __shared__ __attribute__((aligned(16))) float sL[NS][BM];       // lse * log2(e)
+  __shared__ __attribute__((aligned(16))) float sD[NS][BM];       // Delta
 
   const Item it = items[blockIdx.x];
   const int tid = threadIdx.x;
@@ -104,24 +140,37 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
   const int64_t lbase = static_cast<int64_t>(it.head) * T + it.row0;
   const bf16* qh = q + base;
   const bf16* gh = dout + base;
-  const float* l2h = lse2 + lbase;
-  const float* dlh = delta + lbase;
+  const float* vec_src = (wave < NW / 2 ? lse2 : delta) + lbase;
+  const int vec_off = (wave % (NW / 2)) * 32;
   const int key_wave0 = it.tile0 + wave * 32;
   const bool wave_active = key_wave0 < L;
 
-  auto stage = [&](int b, int i0) {
+  // Every wave issues exactly kOps DMA instructions per stage, so counted waits work.
+  auto stage = [&](int t) {
+    const int b = t % NS, i0 = t * BM;
     tile_dma<D, BM, kThreads>(sQ[b], qh, rs, i0, L, tid);
     tile_dma<D, BM, kThreads>(sG[b], gh, rs, i0, L, tid);
-    // BM floats of lse2 and of Delta, 64 per wave instruction (lanes past BM idle).
-#pragma unroll
-    for (int j = wave; j < 2 * ((BM + 63) / 64); j += kThreads / 64) {
-      const int half = (BM + 63) / 64;
-      const int part = j < half ? j : j - half;
-      if (part * 64 + lane < BM)
-        rows64_dma((j < half ? sL[b] : sD[b]) + part * 64, j < half ? l2h : dlh, i0 + part * 64, L, lane);
+    float* dst = (wave < NW / 2 ? sL[b] : sD[b]) + vec_off;
+    if (lane < 32) rows64_dma(dst, vec_src, i0 + vec_off, L, lane);
+  };
+  // Before reading stage t + 1: wait for it, leaving the stages issued after it in flight.
+  auto wait_next = [&](int t, int ntiles) {
+    const int after = min(NS - 2, ntiles - 2 - t);  // stages issued after t + 1
+    if (after >= NS - 2) {
+      wait_vmcnt<(NS - 2) * kOps>();
+    } else if (NS > 3 && after == 1) {
+      wait_vmcnt<kOps>();
+    } else if (NS > 4 && after == 2) {
+      wait_vmcnt<2 * kOps>();
+    } else {
+      wait_vmcnt0();
     }
   };
-  stage(0, 0);
+  static_assert(NS >= 2 && NS <= 5, "wait_next handles up to 3 stages in flight");
+
+  const int ntiles = (L + BM - 1) / BM;
+  const int nfull = L / BM;
+  stage(0);
 
   // K and V of this wave's 32 keys, as B operands (lane = key, elements along head dim).
   bf16x8 kop[KK], vop[KK];
@@ -140,16 +189,20 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
     dka[db] = zero16();
     dva[db] = zero16();
   }
+  // Stage 0 and the K / V loads complete here; a wait the compiler sees also keeps it
+  // from waiting for the K / V loads inside the loop (where the stages it does not see
+  // would make that a full wait).
+  wait_vmcnt0();
+#pragma unroll
+  for (int t = 1; t < NS - 1; ++t)
+    if (t < ntiles) stage(t);
+  __syncthreads();
 
-  const int ntiles = (L + BM - 1) / BM;
-  const int nfull = L / BM;
   const uint32_t oo = opnd_lane_off<D>(lane);
   const uint32_t ro0 = rows_lane_off<D>(lane, 0), ro1 = rows_lane_off<D>(lane, 1);
-  wait_vmcnt0();
-  __syncthreads();
   for (int tt = 0; tt < nfull; ++tt) {
-    const int b = tt & 1;
-    if (tt + 1 < ntiles) stage(b ^ 1, (tt + 1) * BM);
+    const int b = tt % NS;
+    if (tt + NS - 1 < ntiles) stage(tt + NS - 1);
     if (wave_active) {
       const uint32_t tq = lds_addr(sQ[b]), tg = lds_addr(sG[b]);
       const uint32_t qb = tq + oo, gb = tg + oo;
@@ -158,11 +211,11 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
       for (int qs = 0; qs < BM; qs += 32)
         dkdv_step<D, false>(qb, gb, q0, q1, g0, g1, sL[b], sD[b], qs, 32, c, kop, vop, dka, dva, lane);
     }
-    wait_vmcnt0();
+    wait_next(tt, ntiles);
     __syncthreads();
   }
   if (nfull < ntiles && wave_active) {  // last tile, 1 .. BM-1 queries
-    const int b = nfull & 1;
+    const int b = nfull % NS;
     const int rem = L - nfull * BM;
     const uint32_t tq = lds_addr(sQ[b]), tg = lds_addr(sG[b]);
     const uint32_t qb = tq + oo, gb = tg + oo;

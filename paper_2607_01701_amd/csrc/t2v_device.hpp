@@ -109,12 +109,30 @@ T2V_DEV int swz_off(int r, int col) {
 
 typedef __attribute__((address_space(3))) void lds_void;
 
+// LDS DMA (global_load_lds) of 16 or 4 bytes per lane: lane i writes LDS bytes
+// [lds + W i, lds + W (i + 1)) with W = 16 or 4; `lds` must be wave-uniform (it goes to M0).
+//
+// Written as inline assembly on purpose: for the compiler's builtin form, the wait-count
+// pass cannot tell which LDS bytes a DMA writes, so it puts a full vmcnt(0) wait before
+// the next LDS read, which makes every prefetch finish before the current tile's work
+// starts. Here the compiler does not see the DMA at all, and the kernels order it
+// themselves with counted vmcnt waits before the barrier that publishes a stage. (The
+// compiler's own waits for ordinary loads stay correct: unseen DMAs only make them wait
+// longer.) The s_nop covers the M0-write to LDS-DMA hazard.
+T2V_DEV void dma_lds16(const void* g, uint32_t lds) {
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(lds) : "memory");
+}
+T2V_DEV void dma_lds4(const void* g, uint32_t lds) {
+  asm volatile("s_nop 0\n\tglobal_load_lds_dword %0, off" ::"v"(g), "{m0}"(lds) : "memory");
+}
+
 // Asynchronous copy of rows row0 .. row0 + R - 1 of one (clip, head) into a swizzled LDS
 // tile with global_load_lds_dwordx4 (each wave instruction fills 1 KB of LDS; lane i the
 // 16 bytes at offset 16 i). Rows at or past `L` are replaced by row L - 1, so the tile only
 // ever holds finite input values; callers mask those rows. `g` points at token 0 of the
-// clip for this head; `rs` is the token stride in elements. Completion must be awaited
-// with wait_vmcnt0() before a barrier that precedes reads of the tile.
+// clip for this head; `rs` is the token stride in elements. Each wave issues R * D / 512 /
+// (NTHREADS / 64) DMA instructions; completion must be awaited with a vmcnt wait before a
+// barrier that precedes reads of the tile.
 template <int D, int R, int NTHREADS>
 T2V_DEV void tile_dma(bf16* tile, const bf16* g, int64_t rs, int row0, int L, int tid) {
   constexpr int CPR = D / 8;          // chunks per row
@@ -122,19 +140,27 @@ T2V_DEV void tile_dma(bf16* tile, const bf16* g, int64_t rs, int row0, int L, in
   constexpr int NI = R / RPI;         // wave instructions per tile
   constexpr int NW = NTHREADS / 64;
   static_assert(R % RPI == 0 && NI % NW == 0, "tile shape must fill whole wave instructions");
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: no exec-mask branches
   const int lane = tid & 63;
 #pragma unroll
   for (int i = wave; i < NI; i += NW) {
     const int r = i * RPI + lane / CPR;
     const int c = (lane % CPR) ^ swz<D>(r);
     const int gr = min(row0 + r, L - 1);
-    __builtin_amdgcn_global_load_lds(g + gr * rs + c * 8, (lds_void*)(tile + i * 512), 16, 0, 0);
+    dma_lds16(g + gr * rs + c * 8, static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void*)(tile + i * 512))));
   }
 }
 
 // Waits until this thread's outstanding vector memory operations (including LDS DMA) are done.
 T2V_DEV void wait_vmcnt0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// Waits until at most N of this thread's vector memory operations are outstanding. They
+// complete in issue order, so this waits for everything issued before the last N.
+template <int N>
+T2V_DEV void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt is a 6-bit field");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
 
 // 16-byte operand read of logical chunk `chunk` of row r from a swizzled tile.
 template <int D>
