@@ -49,6 +49,9 @@ def parse_args():
     ap.add_argument("--workload", default="hetero", help="tiny | uniform | hetero | long | skew")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sweep", action="store_true",
+                    help="time every workload (and the natural-order scheduler ablation on the mixed ones); "
+                         "one JSON line per run, no CPU baseline")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain device copy of known size (for HBM counter scaling)")
     ap.add_argument("--ingest-rocpd", nargs=5, metavar=("KT_DB", "FETCH_DB", "WRITE_DB", "COPY_FETCH_DB",
@@ -196,33 +199,21 @@ def ingest_rocpd(kt_db, fetch_db, write_db, copy_fetch_db, copy_write_db, worklo
     print("\n".join(lines))
 
 
-def main():
-    args = parse_args()
-    if args.ingest_rocpd:
-        ingest_rocpd(*args.ingest_rocpd, workload=args.workload)
-        return
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}): libt2vattn "
-              "has no multi-GPU path; sharding across GPUs is not implemented.", file=sys.stderr, flush=True)
-        sys.exit(2)
+def run_workload(workload, seed, steps, warmup, order=None):
+    """Times `steps` fwd+bwd steps of one workload after `warmup` untimed ones; returns the
+    bench record (without the CPU baseline) and the pack."""
     import numpy as np
     import torch
-
-    if not torch.cuda.is_available():
-        print("bench.py needs a GPU", file=sys.stderr)
-        sys.exit(1)
-    if args.copy_calibration:
-        copy_calibration()
-        return
 
     from paper_2607_01701_amd import _lib
     from paper_2607_01701_amd.workload import DESCRIPTIONS, attention_flops, make_workload
 
+    if order is not None:
+        os.environ["T2V_ORDER"] = order  # read by the library at each call
     t_gen = time.perf_counter()
-    pack = make_workload(args.workload, seed=args.seed)
+    pack = make_workload(workload, seed=seed)
     H, D, T = pack.heads, pack.head_dim, pack.total_tokens
-    print(f"[bench] workload {args.workload}: T={T} H={H} D={D} sum(L^2)={pack.sum_sq_len} "
+    print(f"[bench] workload {workload}: T={T} H={H} D={D} sum(L^2)={pack.sum_sq_len} "
           f"(generated in {time.perf_counter() - t_gen:.1f}s)", file=sys.stderr, flush=True)
 
     def dev(bits):
@@ -251,23 +242,23 @@ def main():
         if st:
             raise _lib.T2VError(st, _lib.t2v_last_error())
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-    print(f"[bench] warmup {args.warmup} steps done", file=sys.stderr, flush=True)
+    print(f"[bench] warmup {warmup} steps done", file=sys.stderr, flush=True)
 
     _lib.t2v_timing_enable(True)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     e0.record(stream)
-    for _ in range(args.steps):
+    for _ in range(steps):
         step()
     e1.record(stream)
     torch.cuda.synchronize()
     ktimes = _lib.t2v_kernel_times()
     _lib.t2v_timing_enable(False)
-    ms_step = e0.elapsed_time(e1) / args.steps
-    print(f"[bench] timed {args.steps} steps: {ms_step:.3f} ms/step", file=sys.stderr, flush=True)
+    ms_step = e0.elapsed_time(e1) / steps
+    print(f"[bench] timed {steps} steps: {ms_step:.3f} ms/step", file=sys.stderr, flush=True)
 
     fl = attention_flops(pack)
     tflops = fl["fwd_bwd"] / (ms_step * 1e-3) * 1e-12
@@ -287,7 +278,7 @@ def main():
     if os.path.exists(TRAFFIC_FILE):
         with open(TRAFFIC_FILE) as f:
             rec = json.load(f)
-        if rec.get("kernel_source_hash") == kernel_source_hash() and rec.get("workload") == args.workload:
+        if rec.get("kernel_source_hash") == kernel_source_hash() and rec.get("workload") == workload:
             traffic = rec.get("kernels", {}).get(dominant, {}).get("hbm_bytes_per_launch")
     roofline = {"bound": "mfma", "kernel": dominant, "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
@@ -301,15 +292,15 @@ def main():
         "value": round(tflops, 2),
         "unit": "TFLOP/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+        "steps": steps,
+        "warmup": warmup,
         "ms_per_step": round(ms_step, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic: seeded N(0,1) values rounded to bf16; clip lengths from latent grids (no dataset)",
-        "config": {"workload": f"{args.workload}: {DESCRIPTIONS[args.workload]}", "seed": args.seed,
+        "config": {"workload": f"{workload}: {DESCRIPTIONS[workload]}", "seed": seed,
                    "total_tokens": T, "heads": H, "head_dim": D, "sum_sq_len": pack.sum_sq_len,
                    "clip_lengths": pack.lengths.tolist() if pack.nseq <= 32 else f"{pack.nseq} clips",
                    "flop_convention": "fwd 4*H*D*sum(L^2) + bwd 10*H*D*sum(L^2)"},
@@ -320,6 +311,42 @@ def main():
         "roofline": roofline,
         "kernel_source_hash": kernel_source_hash(),
     }
+    if order is not None:
+        res["config"]["scheduler_order"] = order
+    del q, k, v, g, out, dq, dk, dv, lse, delta
+    torch.cuda.empty_cache()
+    return res, pack
+
+
+def main():
+    args = parse_args()
+    if args.ingest_rocpd:
+        ingest_rocpd(*args.ingest_rocpd, workload=args.workload)
+        return
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}): libt2vattn "
+              "has no multi-GPU path; sharding across GPUs is not implemented.", file=sys.stderr, flush=True)
+        sys.exit(2)
+    import torch
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    if args.copy_calibration:
+        copy_calibration()
+        return
+
+    if args.sweep:
+        # Smaller step counts for the long workloads keep the sweep to about a minute of GPU time.
+        lf = "longest_first"
+        plan = [("tiny", lf, 50), ("uniform", lf, 20), ("hetero", lf, 20), ("long", lf, 5), ("skew", lf, 3),
+                ("hetero", "natural", 20), ("skew", "natural", 3)]
+        for name, order, steps in plan:
+            res, _ = run_workload(name, args.seed, steps, max(1, min(args.warmup, steps // 2)), order)
+            print(json.dumps(res), flush=True)
+        return
+    res, pack = run_workload(args.workload, args.seed, args.steps, args.warmup)
     if not args.no_cpu_baseline:
         print("[bench] timing the float64 oracle on a bounded sample", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(pack)
