@@ -92,7 +92,7 @@ T2V_DEV void dkdv_grad_mfma(const bf16x8 (&pb)[2], const bf16x8 (&sb)[2], uint32
   }
 }
 
-// One whole step (used for the ragged last tile).
+// One 32-query step (full, or the masked last step of a clip).
 template <int D, bool RAGGED>
 T2V_DEV void dkdv_step(uint32_t qbase, uint32_t gbase, uint32_t qr0, uint32_t qr1, uint32_t gr0, uint32_t gr1,
                        const float* sL2, const float* sDl, int qs, int nvalid,
