@@ -57,6 +57,9 @@ def parse_args():
     ap.add_argument("--workload", default="hetero", help="tiny | uniform | hetero | long | skew")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--write-summaries", nargs="+", metavar=("BENCH_JSON", "SWEEP_JSONL"),
+                    help="write the text summaries under profiles/ from a bench line, profiles/hbm_traffic.json "
+                         "and (optionally) a --sweep output")
     ap.add_argument("--sweep", action="store_true",
                     help="time every workload (and the natural-order scheduler ablation on the mixed ones); "
                          "one JSON line per run, no CPU baseline")
@@ -207,6 +210,103 @@ def ingest_rocpd(kt_db, fetch_db, write_db, copy_fetch_db, copy_write_db, worklo
     print("\n".join(lines))
 
 
+PROFILE_CMDS = """Commands (repo root, GPU box; rocprofv3 writes rocpd SQLite files):
+  rocprofv3 --kernel-trace --stats -d gpurun_out/prof_kt -o kt -- python3 bench.py --steps 20 --warmup 5 --no-cpu-baseline
+  rocprofv3 --pmc FETCH_SIZE -d gpurun_out/pmc_fetch -o f -- python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline
+  rocprofv3 --pmc WRITE_SIZE -d gpurun_out/pmc_write -o w -- python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline
+  rocprofv3 --pmc FETCH_SIZE -d gpurun_out/pmc_copy_fetch -o cf -- python3 bench.py --copy-calibration
+  rocprofv3 --pmc WRITE_SIZE -d gpurun_out/pmc_copy_write -o cw -- python3 bench.py --copy-calibration
+  python3 bench.py --steps 20 --warmup 5 > gpurun_out/bench_hetero.json
+Summarised with:
+  python3 bench.py --ingest-rocpd gpurun_out/prof_kt/kt_results.db gpurun_out/pmc_fetch/f_results.db \\
+      gpurun_out/pmc_write/w_results.db gpurun_out/pmc_copy_fetch/cf_results.db gpurun_out/pmc_copy_write/cw_results.db
+  python3 bench.py --write-summaries gpurun_out/bench_hetero.json gpurun_out/sweep.jsonl
+"""
+
+
+def write_summaries(bench_json, sweep_jsonl=None):
+    """Text summaries under profiles/ from a bench line, profiles/hbm_traffic.json and a sweep."""
+    with open(bench_json) as f:
+        b = json.loads(f.read().strip().splitlines()[-1])
+    with open(TRAFFIC_FILE) as f:
+        t = json.load(f)
+    if t["kernel_source_hash"] != b["kernel_source_hash"]:
+        raise SystemExit("the counters and the bench line come from different kernel sources")
+    k, bk = t["kernels"], b["kernels"]
+    c = b["config"]
+    H, D, T, ssq = c["heads"], c["head_dim"], c["total_tokens"], c["sum_sq_len"]
+    hds = H * D * ssq
+    alg = {"fwd": 4 * hds, "bwd_dkdv": 8 * hds, "bwd_dq": 6 * hds}
+    head = ("attention forward + backward kernels, heterogeneous mix workload\n"
+            "(16 clips: 6x1,280 + 7x6,912 + 3x20,280 tokens, 24 heads x 128, bf16), one MI355X.\n"
+            f"Kernel source hash (bench.py kernel_source_hash): {t['kernel_source_hash']}\n\n" + PROFILE_CMDS + "\n")
+    order = ("bwd_dkdv", "bwd_dq", "fwd", "bwd_pre")
+    lines = ["rocprofv3 kernel trace: " + head, "kernel-trace averages (ms per launch):"]
+    lines += [f"  {n:10s} {k[n]['trace_avg_ms']:10.4f}" for n in order]
+    lines.append("bench.py live HIP-event averages (separate run of the same sources, "
+                 f"{b['steps']} timed steps):")
+    lines.append("  " + "   ".join(f"{n} {bk[n]['avg_ms']:.3f} ms" for n in order))
+    lines.append(f"Algorithmic MFMA work per launch (H*D*sum(L^2) = {H}*{D}*{ssq:,}):")
+    lines.append("  " + ", ".join(f"{n} {alg[n] / 1e12:.2f} TFLOP" for n in ("fwd", "bwd_dkdv", "bwd_dq")))
+    lines.append("  -> " + ", ".join(f"{n} {alg[n] / (k[n]['trace_avg_ms'] * 1e-3) / 1e12:.0f} TFLOP/s"
+                                    for n in ("fwd", "bwd_dkdv", "bwd_dq")) + " at the trace averages (peak 2500).")
+    lines.append(f"Whole step (bench.py): {b['ms_per_step']:.2f} ms = {b['value']:.0f} TFLOP/s at 14*H*D*sum(L^2).")
+    with open(os.path.join(ROOT, "profiles", "attn_fwd_bwd_hetero_kernel_trace.txt"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+    tb = T * H * D * 2 / 1e6
+    lb = T * H * 4 / 1e6
+    ab = {"fwd": 4 * tb + lb, "bwd_pre": 2 * tb + 3 * lb, "bwd_dkdv": 6 * tb + 2 * lb, "bwd_dq": 5 * tb + 2 * lb}
+    lines = ["rocprofv3 HBM byte counters: " + head,
+             f"Copy calibration: a {t['copy_bytes'] >> 20} MiB device-to-device copy scales FETCH_SIZE by "
+             f"{t['fetch_scale']:.4f} and WRITE_SIZE by {t['write_scale']:.4f}.", "",
+             "HBM bytes per launch (copy-scaled FETCH_SIZE + WRITE_SIZE) against the algorithmic bytes "
+             "(each input read once, each output written once):"]
+    for n in order:
+        lines.append(f"  {n:10s} fetch {k[n]['fetch_bytes'] / 1e9:7.3f} GB  write {k[n]['write_bytes'] / 1e9:7.3f} GB"
+                     f"  total {k[n]['hbm_bytes_per_launch'] / 1e9:7.3f} GB   algorithmic {ab[n] / 1e3:6.3f} GB"
+                     f"   {k[n]['hbm_bytes_per_launch'] / (k[n]['trace_avg_ms'] * 1e-3) / 1e12:5.2f} TB/s")
+    lines += ["Algorithmic: fwd q,k,v,out + lse; bwd_pre out,dout + Delta, lse*log2e (and the lse read);",
+              "bwd_dkdv q,k,v,dout,dk,dv + lse2, Delta; bwd_dq q,k,v,dout,dq + lse2, Delta.",
+              "The MFMA kernels re-read K/V (fwd, dQ) or Q/dO (dK/dV) once per 128-row tile, mostly from L2 and",
+              "the MALL; their HBM rates sit far below the 8 TB/s peak, so they are not bandwidth bound.",
+              "The Delta pass is HBM-bound; its 4-byte [H, T] stores are scattered, one (token, head) row per",
+              "16 lanes."]
+    with open(os.path.join(ROOT, "profiles", "attn_fwd_bwd_hetero_hbm_counters.txt"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+    if sweep_jsonl:
+        with open(sweep_jsonl) as f:
+            rows = [json.loads(x) for x in f if x.strip()]
+        out = ["bench.py --sweep: every workload, fwd + bwd, one MI355X, bf16 in / fp32 accumulate, synthetic "
+               "N(0,1) inputs.", f"Kernel source hash (bench.py kernel_source_hash): {rows[0]['kernel_source_hash']}",
+               "", "Command (repo root, GPU box):", "  python3 bench.py --sweep > gpurun_out/sweep.jsonl",
+               "  python3 bench.py --write-summaries gpurun_out/bench_hetero.json gpurun_out/sweep.jsonl",
+               "(one JSON line per run; warmup = min(10, steps / 2); HIP events on the launch stream)", "",
+               "FLOP convention: fwd 4*H*D*sum(L^2), bwd 10*H*D*sum(L^2), step 14*H*D*sum(L^2); % of the "
+               "2.5 PFLOP/s bf16 dense peak.", "",
+               f"{'workload':9s} {'order':14s} {'steps':>5s} {'ms/step':>10s} {'step TF/s':>10s} {'% peak':>7s} "
+               f"{'fwd TF/s':>9s} {'bwd TF/s':>9s}  kernels fwd / dK,dV / dQ (executed-MFMA TF/s), Delta GB/s"]
+        vals = {}
+        for r in rows:
+            cc, kk = r["config"], r["kernels"]
+            name = cc["workload"].split(":")[0]
+            vals[(name, cc["scheduler_order"])] = r["value"]
+            ks = (f"{kk['fwd']['tflops']:.0f} / {kk['bwd_dkdv']['tflops']:.0f} / {kk['bwd_dq']['tflops']:.0f}, "
+                  f"{kk['bwd_pre']['gbs']:.0f}")
+            out.append(f"{name:9s} {cc['scheduler_order']:14s} {r['steps']:5d} {r['ms_per_step']:10.3f} "
+                       f"{r['value']:10.1f} {100 * r['frac_of_peak']:6.1f}% {r['fwd_tflops']:9.1f} "
+                       f"{r['bwd_tflops']:9.1f}  {ks}")
+        out += ["", "Scheduler ablation (T2V_ORDER=natural vs the default longest-first order):"]
+        for name in ("hetero", "skew"):
+            a_, n_ = vals.get((name, "longest_first")), vals.get((name, "natural"))
+            if a_ and n_:
+                out.append(f"  {name:7s} {a_:.1f} vs {n_:.1f} TFLOP/s ({100 * (a_ / n_ - 1):+.1f}% for longest-first)")
+        out.append("The tiny pack (640 tokens, 2 heads) is launch-bound: four launches take ~0.08 ms in all.")
+        with open(os.path.join(ROOT, "profiles", "attn_all_workloads_sweep.txt"), "w") as f:
+            f.write("\n".join(out) + "\n")
+
+
 def run_workload(workload, seed, steps, warmup, order=None):
     """Times `steps` fwd+bwd steps of one workload after `warmup` untimed ones; returns the
     bench record (without the CPU baseline) and the pack."""
@@ -330,6 +430,9 @@ def main():
     args = parse_args()
     if args.ingest_rocpd:
         ingest_rocpd(*args.ingest_rocpd, workload=args.workload)
+        return
+    if args.write_summaries:
+        write_summaries(*args.write_summaries[:2])
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:

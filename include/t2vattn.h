@@ -64,7 +64,8 @@ typedef enum {
 /* Forward pass: out = softmax(scale * q k^T) v per clip and head, and lse.
  *   q, k, v    device bf16 [T, H, D], 16-byte aligned, read only
  *   cu_seqlens host int32 [nseq + 1]: cu[0] = 0, non-decreasing, cu[nseq] = T < 2^31
- *   nseq       number of clips (>= 0); heads = H (>= 1); head_dim = D in {64, 128}
+ *   nseq       number of clips (>= 0); heads = H (>= 1); head_dim = D in {64, 128};
+ *              H * D <= 2^22 and T * H * D <= 2^40, else T2V_ERR_INVALID_ARG
  *   scale      finite multiplier of q k^T (1/sqrt(D) in the usual case)
  *   out        device bf16 [T, H, D], written; must not overlap any input
  *   lse        device fp32 [H, T], written; natural-log row normaliser

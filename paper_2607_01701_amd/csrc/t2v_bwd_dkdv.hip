@@ -12,10 +12,12 @@ constexpr int kDkdvBM = 64;     // queries per LDS stage (a multiple of 32)
 constexpr int kDkdvStages = 4;  // LDS stages: up to 3 tiles of Q / dO in flight during one tile's work
 
 // Asynchronous copy of consecutive floats into LDS, one per active lane of the calling
-// wave (lane i copies row row0 + i, clamped to L - 1, to lds[i]).
-T2V_DEV void rows64_dma(float* lds, const float* g, int row0, int L, int lane) {
-  const int r = min(row0 + lane, L - 1);
-  dma_lds4(g + r, static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void*)lds)));
+// wave: lane i copies row i0 + off + i, clamped to L - 1, to lds[i]. The tile's first row
+// i0 must be inside the clip (i0 < L); off + i may run past it, so the clamp is taken
+// relative to i0 and the offset stays in [0, L - 1 - i0].
+T2V_DEV void rows64_dma(float* lds, const float* g, int i0, int off, int L, int lane) {
+  const uint32_t r = static_cast<uint32_t>(min(off + lane, L - 1 - i0));
+  dma_lds4_s(g + i0, r * 4, static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void*)lds)));
 }
 
 // ------------------------------------------------------------------- backward: dK, dV
@@ -131,7 +133,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
   const Item it = items[blockIdx.x];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int G = lane >> 5;
   const int l32 = lane & 31;
   const int L = it.len;
@@ -146,12 +148,13 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
   const bool wave_active = key_wave0 < L;
 
   // Every wave issues exactly kOps DMA instructions per stage, so counted waits work.
+  const TileDma<D, BM, kThreads> dma(tid, rs);
   auto stage = [&](int t) {
     const int b = t % NS, i0 = t * BM;
-    tile_dma<D, BM, kThreads>(sQ[b], qh, rs, i0, L, tid);
-    tile_dma<D, BM, kThreads>(sG[b], gh, rs, i0, L, tid);
+    dma.copy(sQ[b], qh, rs, i0, L);
+    dma.copy(sG[b], gh, rs, i0, L);
     float* dst = (wave < NW / 2 ? sL[b] : sD[b]) + vec_off;
-    if (lane < 32) rows64_dma(dst, vec_src, i0 + vec_off, L, lane);
+    if (lane < 32) rows64_dma(dst, vec_src, i0, vec_off, L, lane);
   };
   // Before reading stage t + 1: wait for it, leaving the stages issued after it in flight.
   auto wait_next = [&](int t, int ntiles) {

@@ -109,8 +109,18 @@ T2V_DEV int swz_off(int r, int col) {
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-// LDS DMA (global_load_lds) of 16 or 4 bytes per lane: lane i writes LDS bytes
-// [lds + W i, lds + W (i + 1)) with W = 16 or 4; `lds` must be wave-uniform (it goes to M0).
+// A wave-uniform pointer, moved to SGPRs (a no-op when the compiler already keeps it there).
+T2V_DEV const void* uniform_ptr(const void* p) {
+  const uint64_t u = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(u));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(u >> 32));
+  return reinterpret_cast<const void*>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+
+// LDS DMA (global_load_lds) of 16 or 4 bytes per lane from sbase + voff: a wave-uniform
+// 64-bit base in SGPRs plus a per-lane 32-bit byte offset, so a tile's addresses cost no
+// 64-bit vector math. Lane i writes LDS bytes [lds + W i, lds + W (i + 1)), W = 16 or 4;
+// `lds` must be wave-uniform (it goes to M0).
 //
 // Written as inline assembly on purpose: for the compiler's builtin form, the wait-count
 // pass cannot tell which LDS bytes a DMA writes, so it puts a full vmcnt(0) wait before
@@ -118,38 +128,69 @@ typedef __attribute__((address_space(3))) void lds_void;
 // starts. Here the compiler does not see the DMA at all, and the kernels order it
 // themselves with counted vmcnt waits before the barrier that publishes a stage. (The
 // compiler's own waits for ordinary loads stay correct: unseen DMAs only make them wait
-// longer.) The s_nop covers the M0-write to LDS-DMA hazard.
-T2V_DEV void dma_lds16(const void* g, uint32_t lds) {
-  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(lds) : "memory");
+// longer.) The compiler does not look inside the assembly for hazards either: the s_nop
+// gives the 5 wait states a vector memory instruction needs after a VALU write of an SGPR
+// it reads (the base may come from v_readfirstlane), which also covers the M0 write.
+T2V_DEV void dma_lds16_s(const void* sbase, uint32_t voff, uint32_t lds) {
+  asm volatile("s_nop 4\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(uniform_ptr(sbase)), "{m0}"(lds)
+               : "memory");
 }
-T2V_DEV void dma_lds4(const void* g, uint32_t lds) {
-  asm volatile("s_nop 0\n\tglobal_load_lds_dword %0, off" ::"v"(g), "{m0}"(lds) : "memory");
+T2V_DEV void dma_lds4_s(const void* sbase, uint32_t voff, uint32_t lds) {
+  asm volatile("s_nop 4\n\tglobal_load_lds_dword %0, %1" ::"v"(voff), "s"(uniform_ptr(sbase)), "{m0}"(lds)
+               : "memory");
 }
 
 // Asynchronous copy of rows row0 .. row0 + R - 1 of one (clip, head) into a swizzled LDS
 // tile with global_load_lds_dwordx4 (each wave instruction fills 1 KB of LDS; lane i the
 // 16 bytes at offset 16 i). Rows at or past `L` are replaced by row L - 1, so the tile only
-// ever holds finite input values; callers mask those rows. `g` points at token 0 of the
-// clip for this head; `rs` is the token stride in elements. Each wave issues R * D / 512 /
-// (NTHREADS / 64) DMA instructions; completion must be awaited with a vmcnt wait before a
-// barrier that precedes reads of the tile.
+// ever holds finite input values; callers mask those rows. Each wave issues
+// R * D / 512 / (NTHREADS / 64) DMA instructions; completion must be awaited with a vmcnt
+// wait before a barrier that precedes reads of the tile.
+//
+// Wave w's instruction j covers tile rows RPI (w + NW j) .. + RPI - 1. The swizzle depends
+// on the row modulo 16 and RPI * NW is a multiple of 16, so a lane's chunk is the same for
+// every j and its byte offset is one per-lane constant plus a wave-uniform j * RPI * NW * rs;
+// only the clip's last, partial tile needs per-lane clamping.
 template <int D, int R, int NTHREADS>
-T2V_DEV void tile_dma(bf16* tile, const bf16* g, int64_t rs, int row0, int L, int tid) {
-  constexpr int CPR = D / 8;          // chunks per row
-  constexpr int RPI = 64 / CPR;       // rows per wave instruction
-  constexpr int NI = R / RPI;         // wave instructions per tile
-  constexpr int NW = NTHREADS / 64;
+struct TileDma {
+  static constexpr int CPR = D / 8;     // chunks per row
+  static constexpr int RPI = 64 / CPR;  // rows per wave instruction
+  static constexpr int NI = R / RPI;    // wave instructions per tile
+  static constexpr int NW = NTHREADS / 64;
+  static constexpr int NJ = NI / NW;    // instructions per wave
   static_assert(R % RPI == 0 && NI % NW == 0, "tile shape must fill whole wave instructions");
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: no exec-mask branches
-  const int lane = tid & 63;
-#pragma unroll
-  for (int i = wave; i < NI; i += NW) {
-    const int r = i * RPI + lane / CPR;
-    const int c = (lane % CPR) ^ swz<D>(r);
-    const int gr = min(row0 + r, L - 1);
-    dma_lds16(g + gr * rs + c * 8, static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void*)(tile + i * 512))));
+  static_assert((RPI * NW) % 16 == 0, "a lane's swizzled chunk must not depend on the instruction");
+  int wave;       // uniform
+  int r0;         // this lane's row in instruction 0
+  uint32_t col;   // byte offset of its 16-byte chunk within the row
+  uint32_t off0;  // r0 * row bytes + col
+
+  T2V_DEV TileDma(int tid, int64_t rs) {
+    wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lane = tid & 63;
+    r0 = RPI * wave + lane / CPR;
+    col = static_cast<uint32_t>(((lane % CPR) ^ swz<D>(r0)) * 16);
+    off0 = static_cast<uint32_t>(r0) * static_cast<uint32_t>(rs * 2) + col;
   }
-}
+
+  // g: token 0 of the clip for this head; rs: token stride in elements.
+  T2V_DEV void copy(bf16* tile, const bf16* g, int64_t rs, int row0, int L) const {
+    const char* base = reinterpret_cast<const char*>(g + static_cast<int64_t>(row0) * rs);
+    const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void*)tile)) + wave * 1024;
+    const int64_t step = static_cast<int64_t>(RPI * NW) * rs * 2;  // bytes between instructions
+    if (row0 + R <= L) {
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) dma_lds16_s(base + j * step, off0, lds0 + j * NW * 1024);
+    } else {
+      const int last = L - 1 - row0;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const int r = min(r0 + RPI * NW * j, last);
+        dma_lds16_s(base, static_cast<uint32_t>(r) * static_cast<uint32_t>(rs * 2) + col, lds0 + j * NW * 1024);
+      }
+    }
+  }
+};
 
 // Waits until this thread's outstanding vector memory operations (including LDS DMA) are done.
 T2V_DEV void wait_vmcnt0() { __builtin_amdgcn_s_waitcnt(0x0F70); }

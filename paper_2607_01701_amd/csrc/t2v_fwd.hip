@@ -158,8 +158,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
   const int q_wave0 = it.tile0 + wave * QB * 32;
   const bool wave_active = q_wave0 < L;
 
-  tile_dma<D, BN, kThreads>(sK[0], kh, rs, 0, L, tid);
-  tile_dma<D, BN, kThreads>(sV[0], vh, rs, 0, L, tid);
+  const TileDma<D, BN, kThreads> dma(tid, rs);
+  dma.copy(sK[0], kh, rs, 0, L);
+  dma.copy(sV[0], vh, rs, 0, L);
 
   bf16x8 qop[QB][KK];
 #pragma unroll
@@ -189,8 +190,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
   for (int tt = 0; tt < nfull; ++tt) {
     const int b = tt & 1;
     if (tt + 1 < ntiles) {
-      tile_dma<D, BN, kThreads>(sK[b ^ 1], kh, rs, (tt + 1) * BN, L, tid);
-      tile_dma<D, BN, kThreads>(sV[b ^ 1], vh, rs, (tt + 1) * BN, L, tid);
+      dma.copy(sK[b ^ 1], kh, rs, (tt + 1) * BN, L);
+      dma.copy(sV[b ^ 1], vh, rs, (tt + 1) * BN, L);
     }
     if (wave_active) {
       const uint32_t kbase = lds_addr(sK[b]) + ko;

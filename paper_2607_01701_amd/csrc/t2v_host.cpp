@@ -45,9 +45,11 @@ int validate_shape(const int32_t* cu, int nseq, int heads, int head_dim, float s
   }
   const int64_t T = cu[nseq];
   // Element offsets are 64-bit in the kernels; bound T*H*D so byte sizes fit comfortably.
+  // Within one staged tile the kernels address rows with 32-bit byte offsets, which needs
+  // 64 rows of stride H*D to stay far below 2^32 bytes.
   const int64_t elems = T * static_cast<int64_t>(heads) * head_dim;
-  if (heads > (1 << 20) || elems > (int64_t(1) << 40))
-    return set_error(T2V_ERR_INVALID_ARG, "T * heads * head_dim is too large");
+  if (static_cast<int64_t>(heads) * head_dim > (int64_t(1) << 22) || elems > (int64_t(1) << 40))
+    return set_error(T2V_ERR_INVALID_ARG, "heads * head_dim or T * heads * head_dim is too large");
   *total_tokens = T;
   return T2V_OK;
 }

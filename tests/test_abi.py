@@ -85,6 +85,7 @@ INV, UNS = _lib.T2V_ERR_INVALID_ARG, _lib.T2V_ERR_UNSUPPORTED
     ([0, 5], {"out": A}, INV, "overlaps"),
     ([0, 5], {"lse": A + 128 * MB + 16}, INV, "overlaps"),
     ([0, 5], {"heads": 1 << 21}, INV, "too large"),
+    ([0, 5], {"heads": (1 << 15) + 1}, INV, "too large"),  # H * D just above 2^22 at D = 128
 ])
 def test_fwd_validation(cu, kw, status, msg):
     st, err = fwd(cu, **kw)

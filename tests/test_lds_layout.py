@@ -80,3 +80,60 @@ def test_d128_reads_are_bank_conflict_free():
                     s, dh = lane & 15, (lane >> 4) & 1
                     addrs.append(off(D, 4 * G + (s >> 2) + 8 * h, 32 * db + 16 * dh + 4 * (s & 3)))
                 assert banks_conflict_free(addrs, 8)
+
+
+def tile_dma_sources(D, R, nthreads, rs, row0, L):
+    """Byte offsets (from token 0 of the clip) that the TileDma model reads, per (wave, lane, j),
+    with the destination (row, logical chunk) each lands in. Mirrors TileDma::copy."""
+    cpr, rpi = D // 8, 64 // (D // 8)
+    nw = nthreads // 64
+    nj = (R // rpi) // nw
+    out = []
+    for wave in range(nw):
+        for lane in range(64):
+            r0 = rpi * wave + lane // cpr
+            col = ((lane % cpr) ^ swz(D, r0)) * 16
+            off0 = r0 * rs * 2 + col
+            for j in range(nj):
+                rj = r0 + rpi * nw * j
+                if row0 + R <= L:
+                    src = row0 * rs * 2 + j * rpi * nw * rs * 2 + off0
+                else:
+                    src = row0 * rs * 2 + min(rj, L - 1 - row0) * rs * 2 + col
+                dst_slot = lane % cpr
+                out.append((src, rj, dst_slot ^ swz(D, rj), wave + nw * j, lane))
+    return out
+
+
+@pytest.mark.parametrize("D", [128, 64])
+@pytest.mark.parametrize("L", [1, 2, 31, 32, 33, 63, 64, 65, 100, 127, 128, 129, 200])
+def test_tile_dma_reads_stay_inside_the_clip(D, L):
+    """Every DMA source row lies in [0, L); a full tile reads exactly its rows; each source is
+    the logical chunk of the row its destination slot holds, as the old per-lane formula did."""
+    H = 24
+    rs = H * D
+    for row0 in range(0, L, 64):
+        seen = set()
+        for src, rj, chunk, instr, lane in tile_dma_sources(D, 64, 256, rs, row0, L):
+            row, rem = divmod(src, rs * 2)
+            assert 0 <= row < L, (row0, rj, row)
+            assert row == min(row0 + rj, L - 1)        # clamped to the clip's last row
+            assert rem == chunk * 16                    # logical chunk of the destination row
+            assert src < 2 ** 32 + row0 * rs * 2       # per-lane part fits 32 bits
+            seen.add((rj, chunk))
+        assert len(seen) == 64 * (D // 8)               # every (row, chunk) of the tile once
+
+
+@pytest.mark.parametrize("L", [1, 2, 17, 31, 32, 33, 40, 63, 64, 65, 96, 97, 130])
+def test_row_statistics_dma_stays_inside_the_clip(L):
+    """rows64_dma: base = row i0 of the tile, lane offset min(off + lane, L - 1 - i0): the row
+    read is in [i0, L - 1] for every piece (off = 0 or 32) and lane, including pieces that
+    start past the clip's end in a short last tile."""
+    for i0 in range(0, L, 64):
+        for off in (0, 32):
+            for lane in range(32):
+                r = min(off + lane, L - 1 - i0)
+                assert r >= 0
+                assert i0 <= i0 + r <= L - 1
+                if i0 + off + lane < L:
+                    assert i0 + r == i0 + off + lane
