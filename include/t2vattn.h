@@ -81,7 +81,7 @@ int t2v_attn_fwd(const void* q, const void* k, const void* v,
  *   dout       device bf16 [T, H, D], the gradient of the loss w.r.t. out
  *   dq, dk, dv device bf16 [T, H, D], written; must not overlap each other or any input
  *   delta_ws   device fp32 [2, H, T], caller-owned scratch (8 * H * T bytes): receives
- *              Delta = rowsum(dout * out) in [0] and lse * log2(e) in [1]
+ *              -Delta = -rowsum(dout * out) in [0] and lse * log2(e) in [1]
  *   stream     hipStream_t to launch on
  * Deterministic: no atomics; repeated calls give bitwise-equal results.
  */

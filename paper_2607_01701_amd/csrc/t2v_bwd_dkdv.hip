@@ -31,32 +31,30 @@ T2V_DEV void dkdv_read_scores(uint32_t qbase, uint32_t gbase, int qs, bf16x8 (&a
   for (int kk = 0; kk < D / 16; ++kk) ag[kk] = read_opnd<D>(gbase, qs, kk);
 }
 
-// S and dP of one 32-query step for this wave's 32 keys (32 queries x 32 keys): lane =
-// key, register r = query qs + 8 (r/4) + 4 G + r % 4.
+// S and dP - Delta of one 32-query step for this wave's 32 keys (32 queries x 32 keys):
+// lane = key, register r = query qs + 8 (r/4) + 4 G + r % 4. dp arrives holding -Delta of
+// each query (the accumulator's initial value), so the product lands on dP - Delta.
 template <int D>
 T2V_DEV void dkdv_scores_mfma(const bf16x8 (&aq)[D / 16], const bf16x8 (&ag)[D / 16], const bf16x8 (&kop)[D / 16],
                               const bf16x8 (&vop)[D / 16], f32x16& s, f32x16& dp) {
   s = zero16();
-  dp = zero16();
 #pragma unroll
   for (int kk = 0; kk < D / 16; ++kk) s = mfma(aq[kk], kop[kk], s);
 #pragma unroll
   for (int kk = 0; kk < D / 16; ++kk) dp = mfma(ag[kk], vop[kk], dp);
 }
 
-// P = exp2(c S - lse2) and dS = P (dP - Delta) of one step, in bf16 by 16-query half.
+// P = exp2(c S - lse2) and dS = P (dP - Delta) of one step (dp holds dP - Delta), in bf16
+// by 16-query half.
 // RAGGED: only the first nvalid queries of the step are inside the clip (their P is
 // forced to zero).
 template <bool RAGGED>
 T2V_DEV void dkdv_softmax(f32x16 s, f32x16 dp, const float* sL2, const float* sDl, int qs, int nvalid, float c,
                           bf16x8 (&pb)[2], bf16x8 (&sb)[2], int lane) {
   const int G = lane >> 5;
-  f32x4 lv[4], dl[4];
+  f32x4 lv[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    lv[i] = *reinterpret_cast<const f32x4*>(sL2 + qs + i * 8 + G * 4);
-    dl[i] = *reinterpret_cast<const f32x4*>(sDl + qs + i * 8 + G * 4);
-  }
+  for (int i = 0; i < 4; ++i) lv[i] = *reinterpret_cast<const f32x4*>(sL2 + qs + i * 8 + G * 4);
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     float p = __builtin_amdgcn_exp2f(fmaf(s[r], c, -lv[r >> 2][r & 3]));
@@ -65,7 +63,7 @@ T2V_DEV void dkdv_softmax(f32x16 s, f32x16 dp, const float* sL2, const float* sD
       p = qi < nvalid ? p : 0.0f;
     }
     s[r] = p;
-    dp[r] = p * (dp[r] - dl[r >> 2][r & 3]);
+    dp[r] = p * dp[r];
   }
   pb[0] = to_bf16x8(s, 0);
   pb[1] = to_bf16x8(s, 8);
@@ -74,24 +72,29 @@ T2V_DEV void dkdv_softmax(f32x16 s, f32x16 dp, const float* sL2, const float* sD
 }
 
 // dV += P^T dO and dK += dS^T Q for one step, contracting over the 16 queries of each half.
+// All dV products come first: they need only P, so the dS arithmetic finishes under them
+// before the dK products need it (measured: dK/dV +1-2% against alternating the two).
 template <int D>
 T2V_DEV void dkdv_grad_mfma(const bf16x8 (&pb)[2], const bf16x8 (&sb)[2], uint32_t qr0, uint32_t qr1, uint32_t gr0,
                             uint32_t gr1, int qs, f32x16 (&dka)[D / 32], f32x16 (&dva)[D / 32]) {
   constexpr int DB = D / 32;
+  bf16x8 bg[2][DB], bq[2][DB];
 #pragma unroll
-  for (int hf = 0; hf < 2; ++hf) {
-    bf16x8 bg[DB], bq[DB];
+  for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      bg[db] = read_rows_opnd<D>(gr0, gr1, qs + hf * 16, db);
-      bq[db] = read_rows_opnd<D>(qr0, qr1, qs + hf * 16, db);
-    }
+    for (int db = 0; db < DB; ++db) bg[hf][db] = read_rows_opnd<D>(gr0, gr1, qs + hf * 16, db);
 #pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      dva[db] = mfma(pb[hf], bg[db], dva[db]);
-      dka[db] = mfma(sb[hf], bq[db], dka[db]);
-    }
-  }
+  for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+    for (int db = 0; db < DB; ++db) dva[db] = mfma(pb[hf], bg[hf][db], dva[db]);
+#pragma unroll
+  for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+    for (int db = 0; db < DB; ++db) bq[hf][db] = read_rows_opnd<D>(qr0, qr1, qs + hf * 16, db);
+#pragma unroll
+  for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+    for (int db = 0; db < DB; ++db) dka[db] = mfma(sb[hf], bq[hf][db], dka[db]);
 }
 
 // One 32-query step (full, or the masked last step of a clip).
@@ -104,6 +107,15 @@ T2V_DEV void dkdv_step(uint32_t qbase, uint32_t gbase, uint32_t qr0, uint32_t qr
   __builtin_amdgcn_iglp_opt(0);
   bf16x8 aq[D / 16], ag[D / 16], pb[2], sb[2];
   f32x16 s, dp;
+  {  // dP's accumulator starts at -Delta (stored negated by the preprocess)
+    const int G = lane >> 5;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const f32x4 x = *reinterpret_cast<const f32x4*>(sDl + qs + i * 8 + G * 4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) dp[i * 4 + e] = x[e];
+    }
+  }
   dkdv_read_scores<D>(qbase, gbase, qs, aq, ag);
   dkdv_scores_mfma<D>(aq, ag, kop, vop, s, dp);
   dkdv_softmax<RAGGED>(s, dp, sL2, sDl, qs, nvalid, c, pb, sb, lane);
@@ -113,7 +125,7 @@ T2V_DEV void dkdv_step(uint32_t qbase, uint32_t gbase, uint32_t qr0, uint32_t qr
 template <int D>
 __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
-    const bf16* __restrict__ dout, const float* __restrict__ lse2, const float* __restrict__ delta,
+    const bf16* __restrict__ dout, const float* __restrict__ lse2, const float* __restrict__ ndelta,
     const Item* __restrict__ items, int H, int64_t T, float c, float scale, bf16* __restrict__ dk,
     bf16* __restrict__ dv) {
   constexpr int KK = D / 16;
@@ -122,13 +134,13 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
   constexpr int NS = kDkdvStages;  // LDS stages in flight
   constexpr int NW = kThreads / 64;
   // DMA instructions per wave and stage: the Q and dO tiles, plus one 32-float piece of
-  // lse * log2(e) or Delta.
+  // lse * log2(e) or -Delta.
   constexpr int kOps = 2 * (BM * D / 512) / NW + 1;
-  static_assert(2 * BM == 32 * NW, "each wave stages one 32-float piece of lse2 / Delta");
+  static_assert(2 * BM == 32 * NW, "each wave stages one 32-float piece of lse2 / -Delta");
   __shared__ __attribute__((aligned(1024))) bf16 sQ[NS][BM * D];
   __shared__ __attribute__((aligned(1024))) bf16 sG[NS][BM * D];  // dO
   __shared__ __attribute__((aligned(16))) float sL[NS][BM];       // lse * log2(e)
-  __shared__ __attribute__((aligned(16))) float sD[NS][BM];       // Delta
+  __shared__ __attribute__((aligned(16))) float sD[NS][BM];       // -Delta
 
   const Item it = items[blockIdx.x];
   const int tid = threadIdx.x;
@@ -142,7 +154,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
   const int64_t lbase = static_cast<int64_t>(it.head) * T + it.row0;
   const bf16* qh = q + base;
   const bf16* gh = dout + base;
-  const float* vec_src = (wave < NW / 2 ? lse2 : delta) + lbase;
+  const float* vec_src = (wave < NW / 2 ? lse2 : ndelta) + lbase;
   const int vec_off = (wave % (NW / 2)) * 32;
   const int key_wave0 = it.tile0 + wave * 32;
   const bool wave_active = key_wave0 < L;

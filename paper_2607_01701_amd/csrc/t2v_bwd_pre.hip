@@ -1,4 +1,4 @@
-// Backward preprocess: Delta = rowsum(dO * O) and lse * log2(e) (HBM-bound).
+// Backward preprocess: -Delta = -rowsum(dO * O) and lse * log2(e) (HBM-bound).
 #include "t2v_kernel_common.hpp"
 
 namespace t2v {
@@ -9,12 +9,14 @@ namespace {
 
 // ------------------------------------------------------------------- backward: Delta
 
-// Delta[h, t] = sum_d dO[t, h, d] O[t, h, d]  and  lse2[h, t] = lse[h, t] * log2(e).
+// ndelta[h, t] = -sum_d dO[t, h, d] O[t, h, d]  and  lse2[h, t] = lse[h, t] * log2(e). Delta is
+// stored negated because the dK/dV kernel starts its dP accumulator from it (dP - Delta
+// then costs no subtraction) and the dQ kernel adds it.
 template <int D>
 __global__ __launch_bounds__(kThreads) void attn_bwd_pre_kernel(const bf16* __restrict__ out,
                                                                  const bf16* __restrict__ dout,
                                                                  const float* __restrict__ lse, int64_t rows,
-                                                                 int H, int64_t T, float* __restrict__ delta,
+                                                                 int H, int64_t T, float* __restrict__ ndelta,
                                                                  float* __restrict__ lse2) {
   constexpr int LPR = D / 8;            // lanes per (token, head) row
   constexpr int RPB = kThreads / LPR;   // rows per workgroup step
@@ -31,7 +33,7 @@ __global__ __launch_bounds__(kThreads) void attn_bwd_pre_kernel(const bf16* __re
     if (sub == 0) {
       const int64_t t = row / H;
       const int64_t h = row - t * H;
-      delta[h * T + t] = acc;
+      ndelta[h * T + t] = -acc;
       lse2[h * T + t] = lse[h * T + t] * kLog2e;
     }
   }

@@ -294,16 +294,22 @@ T2V_DEV float half_sum(float x) {
   return __builtin_bit_cast(float, (unsigned)r[0]) + __builtin_bit_cast(float, (unsigned)r[1]);
 }
 
+// NaN-propagating maximum / minimum (v_maximum3_f32 / v_minimum3_f32 on gfx950). Unlike
+// fmaxf / fminf they need no canonicalising copies of operands that come straight from an
+// MFMA, and a NaN score carries through to a NaN output instead of being dropped.
+T2V_DEV float max_nan(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+T2V_DEV float min_nan(float a, float b) { return __builtin_elementwise_minimum(a, b); }
+
 T2V_DEV float half_max(float x) {
   const unsigned u = __builtin_bit_cast(unsigned, x);
   auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
-  return fmaxf(__builtin_bit_cast(float, (unsigned)r[0]), __builtin_bit_cast(float, (unsigned)r[1]));
+  return max_nan(__builtin_bit_cast(float, (unsigned)r[0]), __builtin_bit_cast(float, (unsigned)r[1]));
 }
 
 T2V_DEV float half_min(float x) {
   const unsigned u = __builtin_bit_cast(unsigned, x);
   auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
-  return fminf(__builtin_bit_cast(float, (unsigned)r[0]), __builtin_bit_cast(float, (unsigned)r[1]));
+  return min_nan(__builtin_bit_cast(float, (unsigned)r[0]), __builtin_bit_cast(float, (unsigned)r[1]));
 }
 
 }  // namespace t2v

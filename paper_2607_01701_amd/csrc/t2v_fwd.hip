@@ -1,10 +1,10 @@
 // gfx950 kernels for packed variable-length bidirectional attention.
 //
-// One workgroup = 4 waves = 256 threads, one work item (a tile of one clip and one
-// head, from the host scheduler). All products use v_mfma_f32_32x32x16_bf16 with fp32
-// accumulation; K/V (forward, dQ) or Q/dO (dK/dV) tiles are staged through LDS with a
-// two-buffer pipeline: the global loads for tile t+1 are issued before the MFMA work on
-// tile t and land in the other LDS buffer after it, one barrier per tile.
+// One workgroup processes one work item (a tile of one clip and one head, from the host
+// scheduler): 8 waves / 256 queries in the forward and dQ kernels, 4 waves / 128 keys in
+// the dK/dV kernel. All products use v_mfma_f32_32x32x16_bf16 with fp32 accumulation;
+// K/V (forward, dQ) or Q/dO (dK/dV) tiles are staged through LDS ahead of use (two
+// buffers in the forward and dQ kernels, four in dK/dV), one barrier per tile.
 //
 // Forward (paper Section III, Observation 2: full self-attention over each clip):
 // every lane owns one query row of a 32-query block, because scores are computed
@@ -30,6 +30,10 @@ namespace {
 
 constexpr int kFwdQB = 1;  // 32-query blocks per wave
 constexpr int kFwdBN = 64; // keys per LDS stage (a multiple of 32)
+// Eight waves (two per SIMD, 256 queries) share each staged K/V tile, so every tile crosses
+// from L2 into LDS once per 256 queries rather than once per 128 (measured: forward +3-5%
+// against two independent 4-wave workgroups per CU).
+constexpr int kFwdThreads = 512;
 
 // ------------------------------------------------------------------------------ forward
 
@@ -44,15 +48,18 @@ T2V_DEV float tree_sum16(const f32x16& x) {
 }
 
 template <bool NEG>
+T2V_DEV float ext(float a, float b) {
+  return NEG ? min_nan(a, b) : max_nan(a, b);
+}
+
+template <bool NEG>
 T2V_DEV float tree_ext16(const f32x16& x) {
   float a[8];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) a[i] = NEG ? fminf(x[i], x[i + 8]) : fmaxf(x[i], x[i + 8]);
+  for (int i = 0; i < 8; ++i) a[i] = ext<NEG>(x[i], x[i + 8]);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) a[i] = NEG ? fminf(a[i], a[i + 4]) : fmaxf(a[i], a[i + 4]);
-  const float b0 = NEG ? fminf(a[0], a[2]) : fmaxf(a[0], a[2]);
-  const float b1 = NEG ? fminf(a[1], a[3]) : fmaxf(a[1], a[3]);
-  return NEG ? fminf(b0, b1) : fmaxf(b0, b1);
+  for (int i = 0; i < 4; ++i) a[i] = ext<NEG>(a[i], a[i + 4]);
+  return ext<NEG>(ext<NEG>(a[0], a[2]), ext<NEG>(a[1], a[3]));
 }
 
 // One 32-key step of the forward pass for QB query blocks of this wave.
@@ -67,7 +74,6 @@ T2V_DEV void fwd_step(uint32_t kbase, uint32_t vbase0, uint32_t vbase1, int kb, 
   constexpr int KK = D / 16;
   constexpr int DB = D / 32;
   const int G = lane >> 5;
-  const int l32 = lane & 31;
   // S^T (32 keys x 32 queries per block): lane = query, register r = key 8 (r/4) + 4 G + r % 4.
   bf16x8 ka[KK];
 #pragma unroll
@@ -134,7 +140,7 @@ T2V_DEV void fwd_step(uint32_t kbase, uint32_t vbase0, uint32_t vbase1, int kb, 
 }
 
 template <int D, int QB, bool NEG>
-__global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
+__global__ __launch_bounds__(kFwdThreads, 1) void attn_fwd_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
     const Item* __restrict__ items, int H, int64_t T, float c, bf16* __restrict__ out,
     float* __restrict__ lse) {
@@ -158,7 +164,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
   const int q_wave0 = it.tile0 + wave * QB * 32;
   const bool wave_active = q_wave0 < L;
 
-  const TileDma<D, BN, kThreads> dma(tid, rs);
+  const TileDma<D, BN, kFwdThreads> dma(tid, rs);
   dma.copy(sK[0], kh, rs, 0, L);
   dma.copy(sV[0], vh, rs, 0, L);
 
@@ -243,7 +249,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
 
 }  // namespace
 
-int fwd_tile_rows(int) { return (kThreads / 64) * 32 * kFwdQB; }
+int fwd_tile_rows(int) { return (kFwdThreads / 64) * 32 * kFwdQB; }
 
 hipError_t launch_fwd(const AttnArgs& a, void* out, float* lse, const Item* items, int n_items,
                       hipStream_t stream) {
@@ -252,7 +258,7 @@ hipError_t launch_fwd(const AttnArgs& a, void* out, float* lse, const Item* item
   const auto* k = static_cast<const bf16*>(a.k);
   const auto* v = static_cast<const bf16*>(a.v);
   auto* o = static_cast<bf16*>(out);
-  const dim3 grid(n_items), block(kThreads);
+  const dim3 grid(n_items), block(kFwdThreads);
   const bool neg = a.scale < 0.0f;
   if (a.head_dim == 128) {
     if (neg)

@@ -24,7 +24,7 @@ struct AttnArgs {
   void* dq;
   void* dk;
   void* dv;
-  float* delta;  // [2, H, T]: Delta, then lse * log2(e)
+  float* delta;  // [2, H, T]: -Delta, then lse * log2(e)
   int heads;
   int head_dim;
   int64_t total_tokens;
