@@ -63,6 +63,10 @@ def parse_args():
     ap.add_argument("--sweep", action="store_true",
                     help="time every workload (and the natural-order scheduler ablation on the mixed ones); "
                          "one JSON line per run, no CPU baseline")
+    ap.add_argument("--cost-model", action="store_true",
+                    help="sweep uniform buckets (B clips of S tokens) for three model shapes, fit the attention term "
+                         "of the DiT latency model (alpha_2 B S^2 + alpha_1 B S + c0, k = 1) and check it on held-out "
+                         "mixed packs; prints a text report")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain device copy of known size (for HBM counter scaling)")
     ap.add_argument("--ingest-rocpd", nargs=5, metavar=("KT_DB", "FETCH_DB", "WRITE_DB", "COPY_FETCH_DB",
@@ -307,6 +311,119 @@ def write_summaries(bench_json, sweep_jsonl=None):
             f.write("\n".join(out) + "\n")
 
 
+# Model shapes of the paper's Table II (hidden size / heads = head_dim): 1536/12, 3072/24, 1920/30.
+COST_SHAPES = ((12, 128), (24, 128), (30, 64))
+COST_SEQ = (1024, 2048, 4096, 8192, 16384, 32768)
+COST_BATCH = (1, 2, 4, 8)
+COST_MAX_TOKENS = 65536
+
+
+def cost_model_sweep(steps: int = 4, warmup: int = 2):
+    """Time fwd+bwd of libt2vattn on uniform buckets and mixed packs; fit and validate the
+    attention latency model (paper Section IV-B, Eq. (9), the alpha_2 B S^2 term at k = 1)."""
+    import numpy as np
+    import torch
+
+    from paper_2607_01701_amd import _lib, costmodel
+    from paper_2607_01701_amd.workload import cu_from_lengths, workload_shape
+
+    L = _lib.lib()
+    stream = torch.cuda.current_stream()
+    sh = stream.cuda_stream
+    rng = np.random.default_rng(0)
+    heldout = []  # mixed packs: the hetero mix at four seeds, skewed mixes, one long clip
+    for seed in range(4):
+        heldout.append(("hetero seed %d" % seed, workload_shape("hetero", seed)[1]))
+    heldout.append(("1 x 75,600 (21x45x80)", [75600]))
+    heldout.append(("20,280 + 32 x 1,024", [20280] + [1024] * 32))
+    heldout.append(("random 1k-16k x 12", rng.integers(1024, 16385, size=12).tolist()))
+
+    def time_pack(lengths, H, D, bufs):
+        cu = np.ascontiguousarray(cu_from_lengths(lengths), dtype=np.int32)
+        T, nseq = int(cu[-1]), len(lengths)
+        cup = cu.ctypes.data_as(_lib._i32p)
+        q, k, v, g, out, dq, dk, dv, lse, ws = bufs
+        sc = 1.0 / D ** 0.5
+
+        def step():
+            st = L.t2v_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), cup, nseq, H, D, sc, out.data_ptr(),
+                                lse.data_ptr(), sh)
+            if st:
+                raise _lib.T2VError(st, _lib.t2v_last_error())
+            st = L.t2v_attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(), cup, nseq,
+                                H, D, sc, g.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), ws.data_ptr(), sh)
+            if st:
+                raise _lib.T2VError(st, _lib.t2v_last_error())
+
+        for _ in range(warmup):
+            step()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(steps):
+            step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    fit_samples, val_samples = [], []
+    lines = []
+    for H, D in COST_SHAPES:
+        tmax = max(COST_MAX_TOKENS, max(sum(l) for _, l in heldout))
+        gen = torch.Generator(device="cuda").manual_seed(H * 1000 + D)
+        bufs = [torch.randn((tmax, H, D), generator=gen, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+                for _ in range(4)]
+        bufs += [torch.empty((tmax, H, D), dtype=torch.bfloat16, device="cuda") for _ in range(4)]
+        bufs += [torch.empty((H, tmax), dtype=torch.float32, device="cuda"),
+                 torch.empty((2, H, tmax), dtype=torch.float32, device="cuda")]
+        for S in COST_SEQ:
+            for B in COST_BATCH:
+                if B * S > COST_MAX_TOKENS:
+                    continue
+                ms = time_pack([S] * B, H, D, bufs)
+                fit_samples.append(([S] * B, H, D, ms))
+                print(f"[cost-model] H={H} D={D} B={B} S={S}: {ms:.3f} ms", file=sys.stderr, flush=True)
+        for name, lengths in heldout:
+            ms = time_pack(lengths, H, D, bufs)
+            val_samples.append((lengths, H, D, ms, name))
+            print(f"[cost-model] H={H} D={D} {name}: {ms:.3f} ms", file=sys.stderr, flush=True)
+        del bufs
+        torch.cuda.empty_cache()
+
+    # One fit per model shape: the kernels' efficiency differs between head dims (the paper
+    # likewise fits its regression coefficients for the model being trained).
+    lines.append("Attention term of the DiT latency model (Section IV-B, Eq. (9)) on one MI355X (k = 1),")
+    lines.append("fwd + bwd of libt2vattn in bf16, fitted per model shape of Table II:")
+    lines.append("  t_ms = alpha2 * sum(L^2) + alpha1 * sum(L) + c0   (a bucket of B clips of S tokens: sum(L^2) = B*S^2)")
+    lines.append(f"  fit set: uniform buckets, S in {list(COST_SEQ)}, B in {list(COST_BATCH)}, B*S <= {COST_MAX_TOKENS}; "
+                 "rows weighted by 1/t (relative error)")
+    lines.append("  held-out set: mixed packs not used in the fit")
+    lines.append("")
+    all_val = []
+    for H, D in COST_SHAPES:
+        fs = [x for x in fit_samples if x[1] == H and x[2] == D]
+        vs = [x for x in val_samples if x[1] == H and x[2] == D]
+        model, stats = costmodel.fit(fs)
+        ve = costmodel.relative_errors(model, [x[:4] for x in vs])
+        all_val.extend(ve.tolist())
+        lines.append(f"H={H} D={D}: alpha2 = {model.alpha2(H, D):.6e} ms/token^2  alpha1 = {model.alpha1(H, D):.6e} "
+                     f"ms/token  c0 = {model.c0:.4f} ms")
+        lines.append(f"  large-S throughput 14*H*D/alpha2 = {14.0 * H * D / (model.alpha2(H, D) * 1e-3) * 1e-12:.0f} "
+                     f"TFLOP/s; fit rms {100 * stats['rms_rel_err']:.2f}% max {100 * stats['max_rel_err']:.2f}%; "
+                     f"held-out rms {100 * float(np.sqrt(np.mean(ve ** 2))):.2f}% max {100 * float(np.max(np.abs(ve))):.2f}%")
+        lines.append("    B      S   measured_ms  predicted_ms  rel_err")
+        for (l, _, _, ms) in fs:
+            pr = model.predict_lengths(l, H, D)
+            lines.append(f"  {len(l):3d} {l[0]:6d}  {ms:11.3f}  {pr:12.3f}  {100 * (pr - ms) / ms:+6.2f}%")
+        for (l, _, _, ms, name), e in zip(vs, ve):
+            lines.append(f"  {name:26s} {ms:11.3f}  {model.predict_lengths(l, H, D):12.3f}  {100 * e:+6.2f}%  (held out)")
+        lines.append("")
+    av = np.asarray(all_val)
+    lines.append(f"All shapes, held-out packs: rms relative error {100 * float(np.sqrt(np.mean(av ** 2))):.2f}%, "
+                 f"max {100 * float(np.max(np.abs(av))):.2f}%")
+    return "\n".join(lines)
+
+
 def run_workload(workload, seed, steps, warmup, order=None):
     """Times `steps` fwd+bwd steps of one workload after `warmup` untimed ones; returns the
     bench record (without the CPU baseline) and the pack."""
@@ -448,6 +565,9 @@ def main():
         copy_calibration()
         return
 
+    if args.cost_model:
+        print(cost_model_sweep(), flush=True)
+        return
     if args.sweep:
         # Smaller step counts for the long workloads keep the sweep to about a minute of GPU time.
         lf = "longest_first"
