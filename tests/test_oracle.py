@@ -431,3 +431,223 @@ def test_key_rows_torch_matches_full():
     for i, j in enumerate(keys):
         assert np.allclose(r["dk"][i], full["dk"][30 + j, 0], atol=1e-13)
         assert np.allclose(r["dv"][i], full["dv"][30 + j, 0], atol=1e-13)
+
+
+# ---------------------------------------------------------------- cross-attention pins
+#
+# Queries of sequence s at rows cu_q[s] .. cu_q[s+1], keys/values at cu_k[s] .. cu_k[s+1]
+# (Wan2.1's cross-attention, Section V-A; text conditioning, Section II-A; text under 256
+# tokens, Section IV-B footnote). Each pin below is fixed by the mathematics, as above.
+
+def rand_cross(lq, lk, H, D, seed):
+    rng = np.random.default_rng(seed)
+    cuq, cuk = cu_from_lengths(lq), cu_from_lengths(lk)
+    q, do = (rng.standard_normal((int(cuq[-1]), H, D)) for _ in range(2))
+    k, v = (rng.standard_normal((int(cuk[-1]), H, D)) for _ in range(2))
+    return cuq, cuk, q, k, v, do
+
+
+def check_cross_one_key(mod):
+    """X1: one key per sequence: out = v0 for every query, lse = s q.k0, dq = dk = 0, dv0 = sum dO."""
+    cuq, cuk, q, k, v, do = rand_cross([5, 3], [1, 1], 2, 8, 21)
+    sc = 0.41
+    r = mod.attention(q, k, v, do, cuq, sc, cu_seqlens_k=cuk)
+    ok = True
+    for s in range(2):
+        a, b, j = cuq[s], cuq[s + 1], cuk[s]
+        ok &= np.allclose(r["out"][a:b], np.broadcast_to(v[j], (b - a,) + v.shape[1:]), atol=1e-14)
+        ok &= np.allclose(r["lse"][:, a:b].T, sc * np.einsum("thd,hd->th", q[a:b], k[j]), atol=1e-13)
+        ok &= np.allclose(r["dv"][j], do[a:b].sum(axis=0), atol=1e-13)
+    ok &= np.all(np.abs(r["dq"]) < 1e-14) and np.all(np.abs(r["dk"]) < 1e-13)
+    return bool(ok)
+
+
+def check_cross_equal_keys(mod):
+    """X2: identical keys: uniform weights over the Lk keys: mean of V, lse = s q.k + ln Lk, dq = 0."""
+    cuq, cuk, q, k, v, do = rand_cross([7], [13], 2, 8, 22)
+    k[:] = k[0]
+    sc = 0.3
+    r = mod.attention(q, k, v, do, cuq, sc, cu_seqlens_k=cuk)
+    ok = np.allclose(r["out"], np.broadcast_to(v.mean(axis=0), q.shape), atol=1e-13)
+    ok &= np.allclose(r["lse"], sc * np.einsum("thd,hd->ht", q, k[0]) + math.log(13), atol=1e-13)
+    ok &= np.all(np.abs(r["dq"]) < 1e-12)
+    return bool(ok)
+
+
+def check_cross_invariants(mod):
+    """X3: per (sequence, head): sum_j dk_j = 0, sum_j dv_j = sum_i dO_i, <Q, dQ> = <K, dK>."""
+    lq, lk = [5, 17, 1, 30], [9, 2, 4, 1]
+    cuq, cuk, q, k, v, do = rand_cross(lq, lk, 3, 8, 23)
+    r = mod.attention(q, k, v, do, cuq, 0.35, cu_seqlens_k=cuk)
+    ok = True
+    for s in range(len(lq)):
+        a, b, ka, kb = cuq[s], cuq[s + 1], cuk[s], cuk[s + 1]
+        for h in range(3):
+            dk, dv, dq = r["dk"][ka:kb, h], r["dv"][ka:kb, h], r["dq"][a:b, h]
+            ok &= np.max(np.abs(dk.sum(0))) < 1e-12
+            ok &= np.allclose(dv.sum(0), do[a:b, h].sum(0), atol=1e-12)
+            ok &= abs(np.sum(q[a:b, h] * dq) - np.sum(k[ka:kb, h] * dk)) < 1e-11
+    return bool(ok)
+
+
+def torch_reference_cross(cuq, cuk, q, k, v, do, sc):
+    """torch SDPA (math path, float64, CPU) with a rectangular block mask + autograd."""
+    import torch
+    segq = np.repeat(np.arange(len(cuq) - 1), np.diff(cuq))
+    segk = np.repeat(np.arange(len(cuk) - 1), np.diff(cuk))
+    mask = torch.from_numpy(segq)[:, None] == torch.from_numpy(segk)[None, :]
+    tq, tk, tv = (torch.tensor(np.ascontiguousarray(x.transpose(1, 0, 2))[None], dtype=torch.float64,
+                               requires_grad=True) for x in (q, k, v))
+    out = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, attn_mask=mask, scale=sc)
+    out.backward(torch.tensor(np.ascontiguousarray(do.transpose(1, 0, 2))[None], dtype=torch.float64))
+    scores = (sc * (tq.detach() @ tk.detach().transpose(-1, -2))).masked_fill(~mask, float("-inf"))
+    lse = torch.logsumexp(scores, dim=-1)[0]
+
+    def back(t):
+        return t[0].detach().numpy().transpose(1, 0, 2)
+
+    return {"out": back(out), "dq": back(tq.grad), "dk": back(tk.grad), "dv": back(tv.grad), "lse": lse.numpy()}
+
+
+def check_cross_torch_sdpa(mod):
+    """X4: agrees with torch's scaled_dot_product_attention + autograd (rectangular mask) to 1e-10."""
+    lq, lk = [3, 1, 16, 7, 33], [5, 4, 1, 20, 9]
+    cuq, cuk, q, k, v, do = rand_cross(lq, lk, 2, 8, 24)
+    sc = 1 / math.sqrt(8)
+    r = mod.attention(q, k, v, do, cuq, sc, cu_seqlens_k=cuk)
+    t = torch_reference_cross(cuq, cuk, q, k, v, do, sc)
+    return all(rel(r[key], t[key]) < 1e-10 for key in ("out", "dq", "dk", "dv", "lse"))
+
+
+def check_cross_finite_differences(mod):
+    """X5: dq, dk, dv of a cross pack equal central differences of <dout, out> (h = 1e-6)."""
+    cuq, cuk, q, k, v, do = rand_cross([3, 1, 4], [2, 5, 1], 2, 4, 25)
+    sc = 0.45
+    r = mod.attention(q, k, v, do, cuq, sc, cu_seqlens_k=cuk)
+
+    def f(qq, kk, vv):
+        return float(np.sum(do * mod.attention(qq, kk, vv, do, cuq, sc, cu_seqlens_k=cuk)["out"]))
+
+    h = 1e-6
+    ok = True
+    for name, arr, pos in (("dq", q, 0), ("dk", k, 1), ("dv", v, 2)):
+        g = np.zeros_like(arr)
+        for ix in np.ndindex(arr.shape):
+            xp, xm = arr.copy(), arr.copy()
+            xp[ix] += h
+            xm[ix] -= h
+            ap, am = [q, k, v], [q, k, v]
+            ap[pos], am[pos] = xp, xm
+            g[ix] = (f(*ap) - f(*am)) / (2 * h)
+        ok &= rel(r[name], g) < 1e-6
+    return bool(ok)
+
+
+def brute_force_cross(cuq, cuk, q, k, v, do, sc):
+    """Pure-Python loops over the cross-attention definition (no BLAS)."""
+    Tq, H, D = q.shape
+    res = {n: np.zeros((Tq, H, D)) for n in ("out", "dq")}
+    res.update({n: np.zeros((k.shape[0], H, D)) for n in ("dk", "dv")})
+    res["lse"] = np.zeros((H, Tq))
+    for s in range(len(cuq) - 1):
+        a, b, ka, kb = int(cuq[s]), int(cuq[s + 1]), int(cuk[s]), int(cuk[s + 1])
+        for h in range(H):
+            for i in range(a, b):
+                srow = [sc * math.fsum(q[i, h, d] * k[j, h, d] for d in range(D)) for j in range(ka, kb)]
+                m = max(srow)
+                e = [math.exp(x - m) for x in srow]
+                z = math.fsum(e)
+                p = [x / z for x in e]
+                res["lse"][h, i] = m + math.log(z)
+                o = [math.fsum(p[j] * v[ka + j, h, d] for j in range(kb - ka)) for d in range(D)]
+                res["out"][i, h] = o
+                dl = math.fsum(do[i, h, d] * o[d] for d in range(D))
+                for j in range(kb - ka):
+                    dp = math.fsum(do[i, h, d] * v[ka + j, h, d] for d in range(D))
+                    ds = p[j] * (dp - dl)
+                    for d in range(D):
+                        res["dq"][i, h, d] += sc * ds * k[ka + j, h, d]
+                        res["dk"][ka + j, h, d] += sc * ds * q[i, h, d]
+                        res["dv"][ka + j, h, d] += p[j] * do[i, h, d]
+    return res
+
+
+def check_cross_brute_force(mod):
+    """X6: the blocked BLAS oracle equals plain loops on a cross pack to 1e-12."""
+    cuq, cuk, q, k, v, do = rand_cross([1, 6, 3], [4, 1, 7], 2, 4, 26)
+    r = mod.attention(q, k, v, do, cuq, 0.55, cu_seqlens_k=cuk)
+    b = brute_force_cross(cuq, cuk, q, k, v, do, 0.55)
+    return all(rel(r[key], b[key]) < 1e-12 for key in ("out", "dq", "dk", "dv", "lse"))
+
+
+CROSS_PINS = {
+    "X1_one_key": check_cross_one_key,
+    "X2_equal_keys": check_cross_equal_keys,
+    "X3_invariants": check_cross_invariants,
+    "X4_torch_sdpa": check_cross_torch_sdpa,
+    "X5_finite_differences": check_cross_finite_differences,
+    "X6_brute_force": check_cross_brute_force,
+}
+
+
+@pytest.mark.parametrize("name", sorted(CROSS_PINS))
+def test_cross_pin(name):
+    assert CROSS_PINS[name](orc), name
+
+
+def test_cross_self_case_is_self_attention():
+    """cu_seqlens_k = cu_seqlens reproduces the self-attention results exactly."""
+    cu, q, k, v, do = rand_pack([9, 4, 1], 2, 8, 27)
+    a = orc.attention(q, k, v, do, cu, 0.4)
+    b = orc.attention(q, k, v, do, cu, 0.4, cu_seqlens_k=cu)
+    for key in ("out", "dq", "dk", "dv", "lse", "delta"):
+        assert np.array_equal(a[key], b[key])
+
+
+def test_cross_rejects_queries_without_keys():
+    cuq, cuk, q, k, v, do = rand_cross([3, 2], [4, 1], 1, 4, 28)
+    with pytest.raises(ValueError):
+        orc.attention(q, k[:4], v[:4], do, cuq, 0.5, cu_seqlens_k=np.array([0, 4, 4]))
+
+
+def test_cross_query_and_key_rows_match_full():
+    """The row- and column-sampled routines follow the key offsets too."""
+    cuq, cuk, q, k, v, do = rand_cross([40, 25], [7, 30], 2, 8, 29)
+    full = orc.attention(q, k, v, do, cuq, 0.3, cu_seqlens_k=cuk)
+    toks, hs = [0, 39, 40, 64], [1, 0, 1, 0]
+    r = orc.query_rows(q, k, v, do, cuq, 0.3, toks, hs, cu_seqlens_k=cuk)
+    for i, (t, h) in enumerate(zip(toks, hs)):
+        assert np.allclose(r["out"][i], full["out"][t, h], atol=1e-13)
+        assert abs(r["lse"][i] - full["lse"][h, t]) < 1e-13
+        assert np.allclose(r["dq"][i], full["dq"][t, h], atol=1e-13)
+    keys = [0, 13, 29]
+    for fn in (orc.key_rows, orc.key_rows_torch):
+        r = fn(q, k, v, do, cuq, 0.3, seq=1, head=1, keys=keys, block_rows=11, cu_seqlens_k=cuk)
+        for i, j in enumerate(keys):
+            assert np.allclose(r["dk"][i], full["dk"][7 + j, 1], atol=1e-13)
+            assert np.allclose(r["dv"][i], full["dv"][7 + j, 1], atol=1e-13)
+
+
+CROSS_MUTANTS = {
+    "keys_at_query_offsets": ("q[a:b, h], k[ka:kb, h], v[ka:kb, h], dout[a:b, h]",
+                              "q[a:b, h], k[a:b, h], v[a:b, h], dout[a:b, h]"),
+    "dk_written_at_query_rows": ('res["dk"][ka:kb, h] = dK', 'res["dk"][a:b, h] = dK[: b - a]'),
+    "dv_written_at_query_rows": ('res["dv"][ka:kb, h] = dV', 'res["dv"][a:b, h] = dV[: b - a]'),
+}
+
+
+@pytest.mark.parametrize("name", sorted(CROSS_MUTANTS) + sorted(MUTANTS))
+def test_cross_mutants_are_caught(name):
+    """Plausible mistakes in the cross-attention plumbing (and the arithmetic mutants above)
+    fail at least one cheap cross pin."""
+    mod = mutant_module(*(CROSS_MUTANTS.get(name) or MUTANTS[name]))
+    failing = []
+    for pin, fn in CROSS_PINS.items():
+        if pin in ("X5_finite_differences", "X6_brute_force"):
+            continue
+        try:
+            if not fn(mod):
+                failing.append(pin)
+        except Exception:
+            failing.append(pin)
+    assert failing, f"mutant {name} passed every cross pin"
