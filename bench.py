@@ -98,21 +98,28 @@ def cpu_baseline(pack, budget_s: float = 15.0):
     except Exception:  # pragma: no cover
         threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
     cu = pack.cu_seqlens
+    cuk = cu if pack.cu_seqlens_k is None else pack.cu_seqlens_k
     lens = np.diff(cu).astype(np.int64)
+    lens_k = np.diff(cuk).astype(np.int64)
     q, k, v, g = (pack.f32(n) for n in ("q", "k", "v", "dout"))
     done, flops, t_used = [], 0.0, 0.0
 
+    def keys_of(s, n):  # self-attention: the (possibly cut) clip itself; cross: the sequence's keys
+        return n if pack.cu_seqlens_k is None else int(lens_k[s])
+
     def run(s, h):
         nonlocal flops, t_used
-        a = int(cu[s])
+        a, ka = int(cu[s]), int(cuk[s])
         n = int(min(lens[s], 8192 if lens[s] > 32768 else lens[s]))
+        nk = keys_of(s, n)
         t0 = time.perf_counter()
-        oracle.head_forward_backward(q[a:a + n, h], k[a:a + n, h], v[a:a + n, h], g[a:a + n, h], pack.scale)
+        oracle.head_forward_backward(q[a:a + n, h], k[ka:ka + nk, h], v[ka:ka + nk, h], g[a:a + n, h], pack.scale)
         dt = time.perf_counter() - t0
         t_used += dt
-        flops += 14.0 * pack.head_dim * float(n) ** 2
+        fl = 14.0 * pack.head_dim * float(n) * float(nk)
+        flops += fl
         done.append((n, h))
-        return dt, 14.0 * pack.head_dim * float(n) ** 2
+        return dt, fl
 
     nz = [int(s) for s in np.argsort(lens, kind="stable") if lens[s] > 0]
     dt, f0 = run(nz[0], 0)
@@ -128,7 +135,7 @@ def cpu_baseline(pack, budget_s: float = 15.0):
         h = (h + 1) % pack.heads
         for s in distinct:
             n = min(lens[s], 8192 if lens[s] > 32768 else lens[s])
-            if 14.0 * pack.head_dim * float(n) ** 2 / rate <= budget_s - t_used:
+            if 14.0 * pack.head_dim * float(n) * float(keys_of(s, int(n))) / rate <= budget_s - t_used:
                 dt, fl = run(s, h)
                 rate = fl / max(dt, 1e-9)
                 progress = True
@@ -136,8 +143,8 @@ def cpu_baseline(pack, budget_s: float = 15.0):
                 break
     return {"value": flops / t_used * 1e-12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
             "seconds": round(t_used, 3),
-            "sample": f"{len(done)} (clip tokens, head) pairs of this workload {done}; float64 numpy oracle "
-                      f"fwd+bwd, counted at the same 14*D*L^2 per pair"}
+            "sample": f"{len(done)} (clip query tokens, head) pairs of this workload {done}; float64 numpy oracle "
+                      f"fwd+bwd, counted at the same 14*D*Lq*Lk per pair"}
 
 
 def copy_calibration():
@@ -438,7 +445,7 @@ def run_workload(workload, seed, steps, warmup, order=None):
     t_gen = time.perf_counter()
     pack = make_workload(workload, seed=seed)
     H, D, T = pack.heads, pack.head_dim, pack.total_tokens
-    print(f"[bench] workload {workload}: T={T} H={H} D={D} sum(L^2)={pack.sum_sq_len} "
+    print(f"[bench] workload {workload}: T={T} H={H} D={D} sum(Lq*Lk)={pack.sum_qk} "
           f"(generated in {time.perf_counter() - t_gen:.1f}s)", file=sys.stderr, flush=True)
 
     def dev(bits):
@@ -446,10 +453,13 @@ def run_workload(workload, seed, steps, warmup, order=None):
 
     q, k, v, g = dev(pack.q), dev(pack.k), dev(pack.v), dev(pack.dout)
     out = torch.empty_like(q)
-    dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(k)
     lse = torch.empty((H, T), dtype=torch.float32, device="cuda")
     delta = torch.empty((2, H, T), dtype=torch.float32, device="cuda")
     cu = np.ascontiguousarray(pack.cu_seqlens, dtype=np.int32)
+    cross = pack.cu_seqlens_k is not None
+    cuk = np.ascontiguousarray(pack.cu_seqlens_k if cross else pack.cu_seqlens, dtype=np.int32)
+    cukp = cuk.ctypes.data_as(_lib._i32p)
     nseq = cu.shape[0] - 1
     L = _lib.lib()
     stream = torch.cuda.current_stream()
@@ -457,13 +467,22 @@ def run_workload(workload, seed, steps, warmup, order=None):
     cup = cu.ctypes.data_as(_lib._i32p)
 
     def step():
-        st = L.t2v_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), cup, nseq, H, D, pack.scale, out.data_ptr(),
-                            lse.data_ptr(), sh)
+        if cross:
+            st = L.t2v_attn_fwd_qk(q.data_ptr(), k.data_ptr(), v.data_ptr(), cup, cukp, nseq, H, D, pack.scale,
+                                   out.data_ptr(), lse.data_ptr(), sh)
+        else:
+            st = L.t2v_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), cup, nseq, H, D, pack.scale,
+                                out.data_ptr(), lse.data_ptr(), sh)
         if st:
             raise _lib.T2VError(st, _lib.t2v_last_error())
-        st = L.t2v_attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(), cup, nseq, H,
-                            D, pack.scale, g.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
-                            delta.data_ptr(), sh)
+        if cross:
+            st = L.t2v_attn_bwd_qk(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(), cup, cukp,
+                                   nseq, H, D, pack.scale, g.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
+                                   delta.data_ptr(), sh)
+        else:
+            st = L.t2v_attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(), cup, nseq,
+                                H, D, pack.scale, g.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
+                                delta.data_ptr(), sh)
         if st:
             raise _lib.T2VError(st, _lib.t2v_last_error())
 
@@ -488,7 +507,7 @@ def run_workload(workload, seed, steps, warmup, order=None):
     fl = attention_flops(pack)
     tflops = fl["fwd_bwd"] / (ms_step * 1e-3) * 1e-12
     avg = {name: (ms / n if n else None) for name, (ms, n) in ktimes.items()}
-    kf = kernel_flops(H, D, pack.sum_sq_len)
+    kf = kernel_flops(H, D, pack.sum_qk)
     kernels = {}
     for name, a in avg.items():
         entry = {"avg_ms": a, "launches": ktimes[name][1]}
@@ -526,9 +545,10 @@ def run_workload(workload, seed, steps, warmup, order=None):
         "dtype": "bf16",
         "data": "synthetic: seeded N(0,1) values rounded to bf16; clip lengths from latent grids (no dataset)",
         "config": {"workload": f"{workload}: {DESCRIPTIONS[workload]}", "seed": seed,
-                   "total_tokens": T, "heads": H, "head_dim": D, "sum_sq_len": pack.sum_sq_len,
+                   "total_tokens": T, "heads": H, "head_dim": D, "sum_sq_len": pack.sum_qk,
                    "clip_lengths": pack.lengths.tolist() if pack.nseq <= 32 else f"{pack.nseq} clips",
-                   "flop_convention": "fwd 4*H*D*sum(L^2) + bwd 10*H*D*sum(L^2)"},
+                   "flop_convention": "fwd 4*H*D*sum(Lq*Lk) + bwd 10*H*D*sum(Lq*Lk) (Lq = Lk = L for "
+                                      "self-attention)"},
         "frac_of_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
         "fwd_tflops": round(fl["fwd"] / (fwd_ms * 1e-3) * 1e-12, 2),
         "bwd_tflops": round(fl["bwd"] / (bwd_ms * 1e-3) * 1e-12, 2),
@@ -536,6 +556,9 @@ def run_workload(workload, seed, steps, warmup, order=None):
         "roofline": roofline,
         "kernel_source_hash": kernel_source_hash(),
     }
+    if cross:
+        res["config"]["key_lengths"] = pack.lengths_k.tolist() if pack.nseq <= 32 else f"{pack.nseq} sequences"
+        res["config"]["total_tokens_k"] = pack.total_tokens_k
     if order is not None:
         res["config"]["scheduler_order"] = order
     del q, k, v, g, out, dq, dk, dv, lse, delta
@@ -571,7 +594,7 @@ def main():
     if args.sweep:
         # Smaller step counts for the long workloads keep the sweep to about a minute of GPU time.
         lf = "longest_first"
-        plan = [("tiny", lf, 50), ("uniform", lf, 20), ("hetero", lf, 20), ("long", lf, 5), ("skew", lf, 3),
+        plan = [("tiny", lf, 50), ("uniform", lf, 20), ("hetero", lf, 20), ("long", lf, 5), ("skew", lf, 3), ("cross", lf, 20),
                 ("hetero", "natural", 20), ("skew", "natural", 3)]
         for name, order, steps in plan:
             res, _ = run_workload(name, args.seed, steps, max(1, min(args.warmup, steps // 2)), order)

@@ -91,6 +91,31 @@ int t2v_attn_bwd(const void* q, const void* k, const void* v,
                  const void* dout, void* dq, void* dk, void* dv, float* delta_ws,
                  void* stream);
 
+/* Cross-attention: queries and keys from separate token streams, e.g. a clip's video tokens
+ * attending to its text tokens. The paper's Wan2.1 model uses self- and cross-attention
+ * (Section V-A), the DiT is conditioned on text (Section II-A), and text sequences are short,
+ * typically under 256 tokens (Section IV-B footnote). For sequence s, queries are rows
+ * cu_seqlens_q[s] .. cu_seqlens_q[s+1] - 1 of q (and of out, lse, dout, dq), keys and values
+ * are rows cu_seqlens_k[s] .. cu_seqlens_k[s+1] - 1 of k and v (and of dk, dv); each query
+ * attends to every key of its sequence. Everything else is as in t2v_attn_fwd / t2v_attn_bwd,
+ * with Tq = cu_seqlens_q[nseq] and Tk = cu_seqlens_k[nseq]:
+ *   q, out, dout, dq   device bf16 [Tq, H, D];   k, v, dk, dv   device bf16 [Tk, H, D]
+ *   lse                device fp32 [H, Tq];      delta_ws       device fp32 [2, H, Tq]
+ *   cu_seqlens_q, cu_seqlens_k   HOST int32 [nseq + 1] each, both validated as cu_seqlens
+ * A sequence must have both queries and keys, or neither (a query without keys has no
+ * softmax): otherwise T2V_ERR_INVALID_ARG. Passing the same array twice is self-attention,
+ * identical to t2v_attn_fwd / t2v_attn_bwd. Deterministic, like them. */
+int t2v_attn_fwd_qk(const void* q, const void* k, const void* v,
+                    const int32_t* cu_seqlens_q, const int32_t* cu_seqlens_k, int nseq,
+                    int heads, int head_dim, float scale, void* out, float* lse, void* stream);
+
+int t2v_attn_bwd_qk(const void* q, const void* k, const void* v,
+                    const void* out, const float* lse,
+                    const int32_t* cu_seqlens_q, const int32_t* cu_seqlens_k, int nseq,
+                    int heads, int head_dim, float scale,
+                    const void* dout, void* dq, void* dk, void* dv, float* delta_ws,
+                    void* stream);
+
 /* Thread-local message describing the last non-OK status of this thread. */
 const char* t2v_last_error(void);
 

@@ -27,8 +27,9 @@ ORDER_NATURAL = 0
 ORDER_LONGEST_FIRST = 1
 
 # Symbols declared in include/t2vattn.h.
-EXPORTS = ("t2v_attn_fwd", "t2v_attn_bwd", "t2v_last_error", "t2v_release_cache", "t2v_build_worklist",
-           "t2v_plan_makespan", "t2v_timing_enable", "t2v_kernel_times", "t2v_version")
+EXPORTS = ("t2v_attn_fwd", "t2v_attn_bwd", "t2v_attn_fwd_qk", "t2v_attn_bwd_qk", "t2v_last_error",
+           "t2v_release_cache", "t2v_build_worklist", "t2v_plan_makespan", "t2v_timing_enable", "t2v_kernel_times",
+           "t2v_version")
 KERNEL_SLOTS = ("fwd", "bwd_pre", "bwd_dkdv", "bwd_dq")
 HOST_EXPORTS = ("t2v_last_error", "t2v_build_worklist", "t2v_plan_makespan", "t2v_version")
 
@@ -61,6 +62,12 @@ def _declare(lib, full: bool):
         lib.t2v_attn_bwd.restype = ctypes.c_int
         lib.t2v_attn_bwd.argtypes = [_vp, _vp, _vp, _vp, _f32p, _i32p, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                      ctypes.c_float, _vp, _vp, _vp, _vp, _f32p, _vp]
+        lib.t2v_attn_fwd_qk.restype = ctypes.c_int
+        lib.t2v_attn_fwd_qk.argtypes = [_vp, _vp, _vp, _i32p, _i32p, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                        ctypes.c_float, _vp, _f32p, _vp]
+        lib.t2v_attn_bwd_qk.restype = ctypes.c_int
+        lib.t2v_attn_bwd_qk.argtypes = [_vp, _vp, _vp, _vp, _f32p, _i32p, _i32p, ctypes.c_int, ctypes.c_int,
+                                        ctypes.c_int, ctypes.c_float, _vp, _vp, _vp, _vp, _f32p, _vp]
         lib.t2v_release_cache.restype = None
         lib.t2v_release_cache.argtypes = []
         lib.t2v_timing_enable.restype = ctypes.c_int
@@ -120,6 +127,21 @@ def t2v_attn_bwd(q, k, v, out, lse, cu_seqlens, nseq, heads, head_dim, scale, do
     cu = _cu_array(cu_seqlens)
     return lib().t2v_attn_bwd(q, k, v, out, lse, cu.ctypes.data_as(_i32p), nseq, heads, head_dim, scale, dout,
                               dq, dk, dv, delta_ws, stream)
+
+
+def t2v_attn_fwd_qk(q, k, v, cu_seqlens_q, cu_seqlens_k, nseq, heads, head_dim, scale, out, lse, stream):
+    """Direct call of t2v_attn_fwd_qk with integer addresses; returns the status."""
+    cq, ck = _cu_array(cu_seqlens_q), _cu_array(cu_seqlens_k)
+    return lib().t2v_attn_fwd_qk(q, k, v, cq.ctypes.data_as(_i32p), ck.ctypes.data_as(_i32p), nseq, heads, head_dim,
+                                 scale, out, lse, stream)
+
+
+def t2v_attn_bwd_qk(q, k, v, out, lse, cu_seqlens_q, cu_seqlens_k, nseq, heads, head_dim, scale, dout, dq, dk, dv,
+                    delta_ws, stream):
+    """Direct call of t2v_attn_bwd_qk with integer addresses; returns the status."""
+    cq, ck = _cu_array(cu_seqlens_q), _cu_array(cu_seqlens_k)
+    return lib().t2v_attn_bwd_qk(q, k, v, out, lse, cq.ctypes.data_as(_i32p), ck.ctypes.data_as(_i32p), nseq, heads,
+                                 head_dim, scale, dout, dq, dk, dv, delta_ws, stream)
 
 
 def t2v_last_error(L=None) -> str:
@@ -183,43 +205,62 @@ def _check_tensor(t, name, T, H, D):
         raise ValueError(f"{name} must be a contiguous CUDA bfloat16 tensor of shape {(T, H, D)}")
 
 
-def attn_fwd(q, k, v, cu_seqlens, scale: float, out=None, lse=None, stream=None):
-    """Forward pass on torch tensors q, k, v [T, H, D] (bf16, on the GPU).
+def attn_fwd(q, k, v, cu_seqlens, scale: float, out=None, lse=None, stream=None, cu_seqlens_k=None):
+    """Forward pass on torch tensors q [Tq, H, D], k, v [Tk, H, D] (bf16, on the GPU).
 
-    Returns (out [T, H, D] bf16, lse [H, T] fp32).
+    cu_seqlens holds the query offsets; cu_seqlens_k the key offsets (None: self-attention,
+    Tk = Tq, t2v_attn_fwd; otherwise t2v_attn_fwd_qk). Returns (out [Tq, H, D] bf16, lse [H, Tq] fp32).
     """
     import torch
     T, H, D = q.shape
-    for name, t in (("q", q), ("k", k), ("v", v)):
-        _check_tensor(t, name, T, H, D)
+    Tk = T if cu_seqlens_k is None else k.shape[0]
+    _check_tensor(q, "q", T, H, D)
+    for name, t in (("k", k), ("v", v)):
+        _check_tensor(t, name, Tk, H, D)
     cu = _cu_array(cu_seqlens)
     if out is None:
         out = torch.empty_like(q)
     if lse is None:
         lse = torch.empty((H, T), dtype=torch.float32, device=q.device)
     L = lib()
-    st = L.t2v_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), cu.ctypes.data_as(_i32p), cu.shape[0] - 1, H, D,
-                        float(scale), out.data_ptr(), lse.data_ptr(), _stream_handle(stream))
+    if cu_seqlens_k is None:
+        st = L.t2v_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), cu.ctypes.data_as(_i32p), cu.shape[0] - 1, H,
+                            D, float(scale), out.data_ptr(), lse.data_ptr(), _stream_handle(stream))
+    else:
+        ck = _cu_array(cu_seqlens_k)
+        st = L.t2v_attn_fwd_qk(q.data_ptr(), k.data_ptr(), v.data_ptr(), cu.ctypes.data_as(_i32p),
+                               ck.ctypes.data_as(_i32p), cu.shape[0] - 1, H, D, float(scale), out.data_ptr(),
+                               lse.data_ptr(), _stream_handle(stream))
     _check(L, st)
     return out, lse
 
 
 def attn_bwd(q, k, v, out, lse, dout, cu_seqlens, scale: float, dq=None, dk=None, dv=None, delta_ws=None,
-             stream=None):
-    """Backward pass; returns (dq, dk, dv) bf16 [T, H, D]."""
+             stream=None, cu_seqlens_k=None):
+    """Backward pass; returns (dq [Tq, H, D], dk, dv [Tk, H, D]) in bf16 (see attn_fwd for cu_seqlens_k)."""
     import torch
     T, H, D = q.shape
-    for name, t in (("q", q), ("k", k), ("v", v), ("out", out), ("dout", dout)):
+    Tk = T if cu_seqlens_k is None else k.shape[0]
+    for name, t in (("q", q), ("out", out), ("dout", dout)):
         _check_tensor(t, name, T, H, D)
+    for name, t in (("k", k), ("v", v)):
+        _check_tensor(t, name, Tk, H, D)
     cu = _cu_array(cu_seqlens)
     dq = torch.empty_like(q) if dq is None else dq
-    dk = torch.empty_like(q) if dk is None else dk
-    dv = torch.empty_like(q) if dv is None else dv
+    dk = torch.empty_like(k) if dk is None else dk
+    dv = torch.empty_like(k) if dv is None else dv
     if delta_ws is None:
         delta_ws = torch.empty((2, H, T), dtype=torch.float32, device=q.device)
     L = lib()
-    st = L.t2v_attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
-                        cu.ctypes.data_as(_i32p), cu.shape[0] - 1, H, D, float(scale), dout.data_ptr(),
-                        dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), delta_ws.data_ptr(), _stream_handle(stream))
+    if cu_seqlens_k is None:
+        st = L.t2v_attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
+                            cu.ctypes.data_as(_i32p), cu.shape[0] - 1, H, D, float(scale), dout.data_ptr(),
+                            dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), delta_ws.data_ptr(), _stream_handle(stream))
+    else:
+        ck = _cu_array(cu_seqlens_k)
+        st = L.t2v_attn_bwd_qk(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
+                               cu.ctypes.data_as(_i32p), ck.ctypes.data_as(_i32p), cu.shape[0] - 1, H, D, float(scale),
+                               dout.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), delta_ws.data_ptr(),
+                               _stream_handle(stream))
     _check(L, st)
     return dq, dk, dv

@@ -45,7 +45,7 @@ int check_host_pointer(const int32_t* cu) {
 
 // Immutable device copies of work lists, keyed by everything that shapes them.
 struct Plan {
-  std::vector<int32_t> cu;
+  std::vector<int32_t> cu, cu_loop;  // offsets of the owned and the looped-over segments
   int heads = 0, block = 0, order = 0, device = 0;
   Item* d_items = nullptr;
   Item* h_items = nullptr;  // pinned source of the upload, kept for the entry's life
@@ -68,7 +68,8 @@ class PlanCache {
  public:
   // Returns the plan (creating and uploading it on `stream` if new) with the
   // upload ordered before any later work on `stream`.
-  int get(const int32_t* cu, int nseq, int heads, int block, int order, hipStream_t stream, Plan** out) {
+  int get(const int32_t* cu, const int32_t* cu_loop, int nseq, int heads, int block, int order, hipStream_t stream,
+          Plan** out) {
     int device = 0;
     hipError_t e = hipGetDevice(&device);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
@@ -77,7 +78,8 @@ class PlanCache {
       Plan& p = **itr;
       if (p.heads == heads && p.block == block && p.order == order && p.device == device &&
           p.cu.size() == static_cast<size_t>(nseq + 1) &&
-          std::memcmp(p.cu.data(), cu, sizeof(int32_t) * (nseq + 1)) == 0) {
+          std::memcmp(p.cu.data(), cu, sizeof(int32_t) * (nseq + 1)) == 0 &&
+          std::memcmp(p.cu_loop.data(), cu_loop, sizeof(int32_t) * (nseq + 1)) == 0) {
         plans_.splice(plans_.begin(), plans_, itr);  // most recently used first
         e = hipStreamWaitEvent(stream, p.ready, 0);
         if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
@@ -87,11 +89,12 @@ class PlanCache {
     }
     std::unique_ptr<Plan> p(new Plan());
     p->cu.assign(cu, cu + nseq + 1);
+    p->cu_loop.assign(cu_loop, cu_loop + nseq + 1);
     p->heads = heads;
     p->block = block;
     p->order = order;
     p->device = device;
-    std::vector<Item> items = build_worklist(cu, nseq, heads, block, order);
+    std::vector<Item> items = build_worklist(cu, cu_loop, nseq, heads, block, order);
     p->n_items = static_cast<int>(items.size());
     const size_t bytes = items.size() * sizeof(Item);
     if (bytes > 0) {
@@ -223,35 +226,105 @@ KernelTimer& timer() {
 }  // namespace
 }  // namespace t2v
 
-extern "C" {
+namespace t2v {
+namespace {
 
-int t2v_attn_fwd(const void* q, const void* k, const void* v, const int32_t* cu_seqlens, int nseq, int heads,
-                 int head_dim, float scale, void* out, float* lse, void* stream) {
-  using namespace t2v;
+// Forward over queries at cu_q and keys at cu_k (the same array for self-attention).
+int attn_fwd_impl(const void* q, const void* k, const void* v, const int32_t* cu_q, const int32_t* cu_k, int nseq,
+                  int heads, int head_dim, float scale, void* out, float* lse, void* stream) {
+  int64_t Tq = 0, Tk = 0;
+  if (cu_q == cu_k) {
+    if (int st = validate_shape(cu_q, nseq, heads, head_dim, scale, &Tq)) return st;
+    Tk = Tq;
+  } else if (int st = validate_shape_qk(cu_q, cu_k, nseq, heads, head_dim, scale, &Tq, &Tk)) {
+    return st;
+  }
+  if (Tq == 0) return T2V_OK;
+  const int64_t qb = tensor_bytes(Tq, heads, head_dim), kb = tensor_bytes(Tk, heads, head_dim);
+  const int64_t lb = Tq * heads * 4;
+  if (int st = validate_pointers({{q, qb, "q"}, {k, kb, "k"}, {v, kb, "v"}}, {{out, qb, "out"}, {lse, lb, "lse"}}))
+    return st;
+  if (int st = check_host_pointer(cu_q)) return st;
+  if (cu_k != cu_q)
+    if (int st = check_host_pointer(cu_k)) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Plan* plan = nullptr;
+  if (int st = cache().get(cu_q, cu_k, nseq, heads, fwd_tile_rows(head_dim), order_from_env(), s, &plan)) return st;
+  if (plan->n_items == 0) return T2V_OK;
+  AttnArgs a{};
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.heads = heads;
+  a.head_dim = head_dim;
+  a.total_tokens = Tq;
+  a.scale = scale;
+  hipError_t e = timer().run(kSlotFwd, s, [&] { return launch_fwd(a, out, lse, plan->d_items, plan->n_items, s); });
+  if (e != hipSuccess) return hip_fail(e, "forward kernel launch");
+  return cache().mark_used(plan, s);
+}
+
+int attn_bwd_impl(const void* q, const void* k, const void* v, const void* out, const float* lse, const int32_t* cu_q,
+                  const int32_t* cu_k, int nseq, int heads, int head_dim, float scale, const void* dout, void* dq,
+                  void* dk, void* dv, float* delta_ws, void* stream) {
+  int64_t Tq = 0, Tk = 0;
+  if (cu_q == cu_k) {
+    if (int st = validate_shape(cu_q, nseq, heads, head_dim, scale, &Tq)) return st;
+    Tk = Tq;
+  } else if (int st = validate_shape_qk(cu_q, cu_k, nseq, heads, head_dim, scale, &Tq, &Tk)) {
+    return st;
+  }
+  if (Tq == 0) return T2V_OK;
+  const int64_t qb = tensor_bytes(Tq, heads, head_dim), kb = tensor_bytes(Tk, heads, head_dim);
+  const int64_t lb = Tq * heads * 4;
+  if (int st = validate_pointers(
+          {{q, qb, "q"}, {k, kb, "k"}, {v, kb, "v"}, {out, qb, "out"}, {lse, lb, "lse"}, {dout, qb, "dout"}},
+          {{dq, qb, "dq"}, {dk, kb, "dk"}, {dv, kb, "dv"}, {delta_ws, 2 * lb, "delta_ws"}}))
+    return st;
+  if (int st = check_host_pointer(cu_q)) return st;
+  if (cu_k != cu_q)
+    if (int st = check_host_pointer(cu_k)) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int order = order_from_env();
+  Plan* pk = nullptr;
+  Plan* pq = nullptr;
+  // dK/dV tiles own keys and loop over queries; dQ tiles own queries and loop over keys.
+  if (int st = cache().get(cu_k, cu_q, nseq, heads, dkdv_tile_rows(head_dim), order, s, &pk)) return st;
+  if (int st = cache().get(cu_q, cu_k, nseq, heads, dq_tile_rows(head_dim), order, s, &pq)) return st;
+  AttnArgs a{};
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.out = out;
+  a.lse = lse;
+  a.dout = dout;
+  a.dq = dq;
+  a.dk = dk;
+  a.dv = dv;
+  a.delta = delta_ws;
+  a.heads = heads;
+  a.head_dim = head_dim;
+  a.total_tokens = Tq;
+  a.scale = scale;
+  hipError_t e = timer().run(kSlotPre, s, [&] { return launch_bwd_pre(a, s); });
+  if (e != hipSuccess) return hip_fail(e, "backward preprocess launch");
+  if (pk->n_items > 0) {
+    e = timer().run(kSlotDkdv, s, [&] { return launch_bwd_dkdv(a, pk->d_items, pk->n_items, s); });
+    if (e != hipSuccess) return hip_fail(e, "dK/dV kernel launch");
+  }
+  if (pq->n_items > 0) {
+    e = timer().run(kSlotDq, s, [&] { return launch_bwd_dq(a, pq->d_items, pq->n_items, s); });
+    if (e != hipSuccess) return hip_fail(e, "dQ kernel launch");
+  }
+  if (int st = cache().mark_used(pk, s)) return st;
+  return cache().mark_used(pq, s);
+}
+
+// Runs f, turning host exceptions into statuses (none may cross the C ABI).
+template <typename F>
+int guarded(F&& f) {
   try {
-    int64_t T = 0;
-    if (int st = validate_shape(cu_seqlens, nseq, heads, head_dim, scale, &T)) return st;
-    if (T == 0) return T2V_OK;
-    const int64_t tb = tensor_bytes(T, heads, head_dim);
-    const int64_t lb = T * heads * 4;
-    if (int st = validate_pointers({{q, tb, "q"}, {k, tb, "k"}, {v, tb, "v"}}, {{out, tb, "out"}, {lse, lb, "lse"}}))
-      return st;
-    if (int st = check_host_pointer(cu_seqlens)) return st;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    Plan* plan = nullptr;
-    if (int st = cache().get(cu_seqlens, nseq, heads, fwd_tile_rows(head_dim), order_from_env(), s, &plan)) return st;
-    if (plan->n_items == 0) return T2V_OK;
-    AttnArgs a{};
-    a.q = q;
-    a.k = k;
-    a.v = v;
-    a.heads = heads;
-    a.head_dim = head_dim;
-    a.total_tokens = T;
-    a.scale = scale;
-    hipError_t e = timer().run(kSlotFwd, s, [&] { return launch_fwd(a, out, lse, plan->d_items, plan->n_items, s); });
-    if (e != hipSuccess) return hip_fail(e, "forward kernel launch");
-    return cache().mark_used(plan, s);
+    return f();
   } catch (const std::bad_alloc&) {
     return set_error(T2V_ERR_OOM, "host allocation failed");
   } catch (...) {
@@ -259,59 +332,46 @@ int t2v_attn_fwd(const void* q, const void* k, const void* v, const int32_t* cu_
   }
 }
 
+}  // namespace
+}  // namespace t2v
+
+extern "C" {
+
+int t2v_attn_fwd(const void* q, const void* k, const void* v, const int32_t* cu_seqlens, int nseq, int heads,
+                 int head_dim, float scale, void* out, float* lse, void* stream) {
+  return t2v::guarded([&] {
+    return t2v::attn_fwd_impl(q, k, v, cu_seqlens, cu_seqlens, nseq, heads, head_dim, scale, out, lse, stream);
+  });
+}
+
 int t2v_attn_bwd(const void* q, const void* k, const void* v, const void* out, const float* lse,
                  const int32_t* cu_seqlens, int nseq, int heads, int head_dim, float scale, const void* dout,
                  void* dq, void* dk, void* dv, float* delta_ws, void* stream) {
-  using namespace t2v;
-  try {
-    int64_t T = 0;
-    if (int st = validate_shape(cu_seqlens, nseq, heads, head_dim, scale, &T)) return st;
-    if (T == 0) return T2V_OK;
-    const int64_t tb = tensor_bytes(T, heads, head_dim);
-    const int64_t lb = T * heads * 4;
-    if (int st = validate_pointers(
-            {{q, tb, "q"}, {k, tb, "k"}, {v, tb, "v"}, {out, tb, "out"}, {lse, lb, "lse"}, {dout, tb, "dout"}},
-            {{dq, tb, "dq"}, {dk, tb, "dk"}, {dv, tb, "dv"}, {delta_ws, 2 * lb, "delta_ws"}}))
-      return st;
-    if (int st = check_host_pointer(cu_seqlens)) return st;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    const int order = order_from_env();
-    Plan* pk = nullptr;
-    Plan* pq = nullptr;
-    if (int st = cache().get(cu_seqlens, nseq, heads, dkdv_tile_rows(head_dim), order, s, &pk)) return st;
-    if (int st = cache().get(cu_seqlens, nseq, heads, dq_tile_rows(head_dim), order, s, &pq)) return st;
-    AttnArgs a{};
-    a.q = q;
-    a.k = k;
-    a.v = v;
-    a.out = out;
-    a.lse = lse;
-    a.dout = dout;
-    a.dq = dq;
-    a.dk = dk;
-    a.dv = dv;
-    a.delta = delta_ws;
-    a.heads = heads;
-    a.head_dim = head_dim;
-    a.total_tokens = T;
-    a.scale = scale;
-    hipError_t e = timer().run(kSlotPre, s, [&] { return launch_bwd_pre(a, s); });
-    if (e != hipSuccess) return hip_fail(e, "backward preprocess launch");
-    if (pk->n_items > 0) {
-      e = timer().run(kSlotDkdv, s, [&] { return launch_bwd_dkdv(a, pk->d_items, pk->n_items, s); });
-      if (e != hipSuccess) return hip_fail(e, "dK/dV kernel launch");
-    }
-    if (pq->n_items > 0) {
-      e = timer().run(kSlotDq, s, [&] { return launch_bwd_dq(a, pq->d_items, pq->n_items, s); });
-      if (e != hipSuccess) return hip_fail(e, "dQ kernel launch");
-    }
-    if (int st = cache().mark_used(pk, s)) return st;
-    return cache().mark_used(pq, s);
-  } catch (const std::bad_alloc&) {
-    return set_error(T2V_ERR_OOM, "host allocation failed");
-  } catch (...) {
-    return set_error(T2V_ERR_INVALID_ARG, "unexpected host exception");
-  }
+  return t2v::guarded([&] {
+    return t2v::attn_bwd_impl(q, k, v, out, lse, cu_seqlens, cu_seqlens, nseq, heads, head_dim, scale, dout, dq, dk,
+                              dv, delta_ws, stream);
+  });
+}
+
+int t2v_attn_fwd_qk(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_q,
+                    const int32_t* cu_seqlens_k, int nseq, int heads, int head_dim, float scale, void* out, float* lse,
+                    void* stream) {
+  return t2v::guarded([&] {
+    if (cu_seqlens_q == nullptr || cu_seqlens_k == nullptr)
+      return t2v::set_error(T2V_ERR_INVALID_ARG, "cu_seqlens_q or cu_seqlens_k is NULL");
+    return t2v::attn_fwd_impl(q, k, v, cu_seqlens_q, cu_seqlens_k, nseq, heads, head_dim, scale, out, lse, stream);
+  });
+}
+
+int t2v_attn_bwd_qk(const void* q, const void* k, const void* v, const void* out, const float* lse,
+                    const int32_t* cu_seqlens_q, const int32_t* cu_seqlens_k, int nseq, int heads, int head_dim,
+                    float scale, const void* dout, void* dq, void* dk, void* dv, float* delta_ws, void* stream) {
+  return t2v::guarded([&] {
+    if (cu_seqlens_q == nullptr || cu_seqlens_k == nullptr)
+      return t2v::set_error(T2V_ERR_INVALID_ARG, "cu_seqlens_q or cu_seqlens_k is NULL");
+    return t2v::attn_bwd_impl(q, k, v, out, lse, cu_seqlens_q, cu_seqlens_k, nseq, heads, head_dim, scale, dout, dq,
+                              dk, dv, delta_ws, stream);
+  });
 }
 
 int t2v_timing_enable(int on) {

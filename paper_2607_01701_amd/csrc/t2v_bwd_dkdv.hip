@@ -148,16 +148,18 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int G = lane >> 5;
   const int l32 = lane & 31;
-  const int L = it.len;
+  const int Lk = it.len;   // keys of the sequence (this tile's rows)
+  const int L = it.llen;   // queries of the sequence (the loop)
   const int64_t rs = static_cast<int64_t>(H) * D;
   const int64_t base = static_cast<int64_t>(it.row0) * rs + static_cast<int64_t>(it.head) * D;
-  const int64_t lbase = static_cast<int64_t>(it.head) * T + it.row0;
-  const bf16* qh = q + base;
-  const bf16* gh = dout + base;
+  const int64_t qbase = static_cast<int64_t>(it.lrow0) * rs + static_cast<int64_t>(it.head) * D;
+  const int64_t lbase = static_cast<int64_t>(it.head) * T + it.lrow0;
+  const bf16* qh = q + qbase;
+  const bf16* gh = dout + qbase;
   const float* vec_src = (wave < NW / 2 ? lse2 : ndelta) + lbase;
   const int vec_off = (wave % (NW / 2)) * 32;
   const int key_wave0 = it.tile0 + wave * 32;
-  const bool wave_active = key_wave0 < L;
+  const bool wave_active = key_wave0 < Lk;
 
   // Every wave issues exactly kOps DMA instructions per stage, so counted waits work.
   const TileDma<D, BM, kThreads> dma(tid, rs);
@@ -191,7 +193,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
   bf16x8 kop[KK], vop[KK];
   {
     const int kj = key_wave0 + l32;
-    const bool ok = kj < L;
+    const bool ok = kj < Lk;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       kop[kk] = load8(k + base + kj * rs + kk * 16 + G * 8, ok);
@@ -249,7 +251,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int kj = key_wave0 + (r >> 2) * 8 + G * 4 + (r & 3);
-      if (kj < L) {
+      if (kj < Lk) {
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
           dk[base + kj * rs + db * 32 + l32] = static_cast<bf16>(dka[db][r] * scale);

@@ -156,13 +156,15 @@ __global__ __launch_bounds__(kFwdThreads, 1) void attn_fwd_kernel(
   const int wave = tid >> 6;
   const int G = lane >> 5;
   const int l32 = lane & 31;
-  const int L = it.len;
+  const int Lq = it.len;   // queries of the sequence (this tile's rows)
+  const int L = it.llen;   // keys of the sequence (the loop)
   const int64_t rs = static_cast<int64_t>(H) * D;  // elements between consecutive tokens
   const int64_t base = static_cast<int64_t>(it.row0) * rs + static_cast<int64_t>(it.head) * D;
-  const bf16* kh = k + base;
-  const bf16* vh = v + base;
+  const int64_t kvbase = static_cast<int64_t>(it.lrow0) * rs + static_cast<int64_t>(it.head) * D;
+  const bf16* kh = k + kvbase;
+  const bf16* vh = v + kvbase;
   const int q_wave0 = it.tile0 + wave * QB * 32;
-  const bool wave_active = q_wave0 < L;
+  const bool wave_active = q_wave0 < Lq;
 
   const TileDma<D, BN, kFwdThreads> dma(tid, rs);
   dma.copy(sK[0], kh, rs, 0, L);
@@ -172,7 +174,7 @@ __global__ __launch_bounds__(kFwdThreads, 1) void attn_fwd_kernel(
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const int qi = q_wave0 + qb * 32 + l32;
-    const bool ok = qi < L;
+    const bool ok = qi < Lq;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) qop[qb][kk] = load8(q + base + qi * rs + kk * 16 + G * 8, ok);
   }
@@ -188,7 +190,7 @@ __global__ __launch_bounds__(kFwdThreads, 1) void attn_fwd_kernel(
   }
 
   const int ntiles = (L + BN - 1) / BN;
-  const int nfull = L / BN;  // tiles with BN keys of the clip
+  const int nfull = L / BN;  // tiles with BN keys of the sequence
   const uint32_t ko = opnd_lane_off<D>(lane);
   const uint32_t vo0 = rows_lane_off<D>(lane, 0), vo1 = rows_lane_off<D>(lane, 1);
   wait_vmcnt0();
@@ -229,7 +231,7 @@ __global__ __launch_bounds__(kFwdThreads, 1) void attn_fwd_kernel(
       const int qi = q_wave0 + qb * 32 + l32;
       const float lt = half_sum(l_run[qb]);
       const float inv = 1.0f / lt;
-      if (qi < L) {
+      if (qi < Lq) {
         bf16* orow = out + base + qi * rs;
 #pragma unroll
         for (int db = 0; db < DB; ++db) {

@@ -54,6 +54,22 @@ int validate_shape(const int32_t* cu, int nseq, int heads, int head_dim, float s
   return T2V_OK;
 }
 
+int validate_shape_qk(const int32_t* cu_q, const int32_t* cu_k, int nseq, int heads, int head_dim, float scale,
+                      int64_t* tq, int64_t* tk) {
+  if (int st = validate_shape(cu_q, nseq, heads, head_dim, scale, tq)) return st;
+  if (cu_k == nullptr) return set_error(T2V_ERR_INVALID_ARG, "cu_seqlens_k is NULL");
+  if (int st = validate_shape(cu_k, nseq, heads, head_dim, scale, tk)) {
+    return set_error(st, std::string("cu_seqlens_k: ") + last_error());
+  }
+  for (int s = 0; s < nseq; ++s) {
+    const bool has_q = cu_q[s + 1] > cu_q[s], has_k = cu_k[s + 1] > cu_k[s];
+    if (has_q != has_k)
+      return set_error(T2V_ERR_INVALID_ARG, "sequence " + std::to_string(s) + (has_q ? " has queries but no keys"
+                                                                                      : " has keys but no queries"));
+  }
+  return T2V_OK;
+}
+
 int validate_pointers(const std::vector<Range>& inputs, const std::vector<Range>& outputs) {
   auto check = [](const Range& r) -> int {
     if (r.ptr == nullptr) return set_error(T2V_ERR_INVALID_ARG, std::string(r.name) + " is NULL");
@@ -85,29 +101,32 @@ namespace {
 
 struct Group {
   int seq, head;
-  int32_t row0, len;
+  int32_t row0, len;    // owned segment
+  int32_t lrow0, llen;  // looped-over segment
   int tiles;
 };
 
-std::vector<Group> make_groups(const int32_t* cu, int nseq, int heads, int block) {
+std::vector<Group> make_groups(const int32_t* cu, const int32_t* cul, int nseq, int heads, int block) {
   std::vector<Group> g;
   for (int s = 0; s < nseq; ++s) {
     const int32_t L = cu[s + 1] - cu[s];
-    if (L <= 0) continue;
+    const int32_t LL = cul[s + 1] - cul[s];
+    if (L <= 0 || LL <= 0) continue;
     const int tiles = (L + block - 1) / block;
-    for (int h = 0; h < heads; ++h) g.push_back({s, h, cu[s], L, tiles});
+    for (int h = 0; h < heads; ++h) g.push_back({s, h, cu[s], L, cul[s], LL, tiles});
   }
   return g;
 }
 
 void append_tiles(std::vector<Item>& out, const Group& g, int t_begin, int t_end, int block) {
-  for (int t = t_begin; t < t_end; ++t) out.push_back({g.row0, g.len, t * block, g.head});
+  for (int t = t_begin; t < t_end; ++t) out.push_back({g.row0, g.len, t * block, g.head, g.lrow0, g.llen, 0, 0});
 }
 
 }  // namespace
 
-std::vector<Item> build_worklist(const int32_t* cu, int nseq, int heads, int block, int order) {
-  std::vector<Group> groups = make_groups(cu, nseq, heads, block);
+std::vector<Item> build_worklist(const int32_t* cu, const int32_t* cu_loop, int nseq, int heads, int block,
+                                 int order) {
+  std::vector<Group> groups = make_groups(cu, cu_loop, nseq, heads, block);
   std::vector<Item> items;
   size_t n = 0;
   for (const auto& g : groups) n += g.tiles;
@@ -116,8 +135,10 @@ std::vector<Item> build_worklist(const int32_t* cu, int nseq, int heads, int blo
     for (const auto& g : groups) append_tiles(items, g, 0, g.tiles, block);
     return items;
   }
-  // Longest clip first; ties keep pack order, so one (clip, head)'s tiles stay adjacent.
-  std::stable_sort(groups.begin(), groups.end(), [](const Group& a, const Group& b) { return a.len > b.len; });
+  // Longest tiles first (a tile costs its rows times the looped-over length; for
+  // self-attention this is the longest clip first); ties keep pack order, so one
+  // (sequence, head)'s tiles stay adjacent.
+  std::stable_sort(groups.begin(), groups.end(), [](const Group& a, const Group& b) { return a.llen > b.llen; });
   // Workgroup b runs on XCD b % 8, and each XCD starts its share in increasing b.
   // Deal whole (clip, head) groups to the least-loaded XCD that still has room, so the
   // concurrently running tiles on one XCD read the same K/V through that XCD's L2,
@@ -140,7 +161,7 @@ std::vector<Item> build_worklist(const int32_t* cu, int nseq, int heads, int blo
         take = std::min(want, cap[best] - q[best].size());
       }
       append_tiles(q[best], g, t, t + static_cast<int>(take), block);
-      load[best] += static_cast<double>(take) * block * g.len;
+      load[best] += static_cast<double>(take) * block * g.llen;
       t += static_cast<int>(take);
     }
   }
@@ -153,7 +174,7 @@ void plan_makespan(const Item* items, int n, int block, int slots, double* makes
   double total = 0.0, largest = 0.0;
   auto cost = [block](const Item& it) {
     const int rows = std::min(block, it.len - it.tile0);
-    return static_cast<double>(rows) * it.len;
+    return static_cast<double>(rows) * it.llen;
   };
   for (int i = 0; i < n; ++i) {
     total += cost(items[i]);
@@ -197,14 +218,19 @@ int t2v_build_worklist(const int32_t* cu_seqlens, int nseq, int heads, int block
   for (int s = 0; s < nseq; ++s)
     if (cu_seqlens[s + 1] < cu_seqlens[s])
       return t2v::set_error(T2V_ERR_INVALID_ARG, "cu_seqlens must be non-decreasing");
-  std::vector<t2v::Item> items = t2v::build_worklist(cu_seqlens, nseq, heads, block, order);
+  std::vector<t2v::Item> items = t2v::build_worklist(cu_seqlens, cu_seqlens, nseq, heads, block, order);
   if (items.size() > static_cast<size_t>(INT32_MAX))
     return t2v::set_error(T2V_ERR_INVALID_ARG, "too many work items");
   *n_items_out = static_cast<int>(items.size());
   if (items_out == nullptr) return T2V_OK;
   if (capacity < static_cast<int>(items.size()))
     return t2v::set_error(T2V_ERR_INVALID_ARG, "capacity too small");
-  std::memcpy(items_out, items.data(), items.size() * sizeof(t2v::Item));
+  for (size_t i = 0; i < items.size(); ++i) {  // self-attention: (row0, len, tile0, head) per item
+    items_out[4 * i + 0] = items[i].row0;
+    items_out[4 * i + 1] = items[i].len;
+    items_out[4 * i + 2] = items[i].tile0;
+    items_out[4 * i + 3] = items[i].head;
+  }
   return T2V_OK;
 }
 
@@ -213,8 +239,12 @@ int t2v_plan_makespan(const int32_t* items, int n_items, int block, int slots, d
   if ((items == nullptr && n_items > 0) || n_items < 0 || block < 1 || slots < 1 || makespan_out == nullptr ||
       lower_bound_out == nullptr)
     return t2v::set_error(T2V_ERR_INVALID_ARG, "bad plan arguments");
-  t2v::plan_makespan(reinterpret_cast<const t2v::Item*>(items), n_items, block, slots, makespan_out,
-                     lower_bound_out);
+  std::vector<t2v::Item> it(static_cast<size_t>(n_items));
+  for (int i = 0; i < n_items; ++i) {  // self-attention items: the loop segment is the clip
+    const int32_t* r = items + 4 * static_cast<size_t>(i);
+    it[i] = {r[0], r[1], r[2], r[3], r[0], r[1], 0, 0};
+  }
+  t2v::plan_makespan(it.data(), n_items, block, slots, makespan_out, lower_bound_out);
   return T2V_OK;
 }
 

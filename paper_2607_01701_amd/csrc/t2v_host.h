@@ -9,14 +9,20 @@
 
 namespace t2v {
 
-// One unit of kernel work: a tile of `block` rows of one (clip, head).
+// One unit of kernel work: a tile of `block` rows of one (sequence, head). A kernel owns
+// the tile's rows (queries in the forward and dQ kernels, keys in the dK/dV kernel) and
+// loops over the sequence's other segment (its keys, or its queries). For self-attention
+// both segments are the clip itself.
 struct Item {
-  int32_t row0;   // first token of the clip in the packed tensor
-  int32_t len;    // clip length L
+  int32_t row0;   // first row of the owned segment in its packed tensor
+  int32_t len;    // owned segment length
   int32_t tile0;  // first row of the tile, relative to row0
   int32_t head;   // head index
+  int32_t lrow0;  // first row of the looped-over segment in its packed tensor
+  int32_t llen;   // looped-over segment length (>= 1 whenever len >= 1)
+  int32_t pad0, pad1;
 };
-static_assert(sizeof(Item) == 16, "Item is one 128-bit load");
+static_assert(sizeof(Item) == 32, "Item is one 256-bit scalar load");
 
 constexpr int kNumXcd = 8;  // MI355X: 8 accelerator dies; workgroups are dealt round-robin
 
@@ -36,11 +42,19 @@ struct Range {
 };
 int validate_pointers(const std::vector<Range>& inputs, const std::vector<Range>& outputs);
 
-// Builds the work list for tiles of `block` rows (see t2v_build_worklist in t2vattn.h).
-std::vector<Item> build_worklist(const int32_t* cu, int nseq, int heads, int block, int order);
+// Validates separate query / key offsets: both as validate_shape (same nseq), and every
+// sequence has either both queries and keys or neither. Stores Tq and Tk.
+int validate_shape_qk(const int32_t* cu_q, const int32_t* cu_k, int nseq, int heads, int head_dim, float scale,
+                      int64_t* tq, int64_t* tk);
+
+// Builds the work list for tiles of `block` rows of the owned segments (offsets cu_own),
+// each looping over the matching segment of cu_loop (see t2v_build_worklist in t2vattn.h;
+// self-attention passes the same offsets twice).
+std::vector<Item> build_worklist(const int32_t* cu_own, const int32_t* cu_loop, int nseq, int heads, int block,
+                                 int order);
 
 // Greedy list-scheduling makespan of `items` on `slots` workers, dealt per XCD when
-// slots is a multiple of kNumXcd. Costs are tile rows x clip length.
+// slots is a multiple of kNumXcd. Costs are tile rows x looped-over length.
 void plan_makespan(const Item* items, int n, int block, int slots, double* makespan, double* lower_bound);
 
 }  // namespace t2v

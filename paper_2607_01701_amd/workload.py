@@ -39,9 +39,10 @@ class Pack:
     head_dim: int
     scale: float
     q: np.ndarray | None = None     # uint16 [T, H, D]
-    k: np.ndarray | None = None
+    k: np.ndarray | None = None     # uint16 [Tk, H, D] (Tk = T unless cu_seqlens_k is set)
     v: np.ndarray | None = None
     dout: np.ndarray | None = None
+    cu_seqlens_k: np.ndarray | None = None  # key offsets for cross-attention; None: self-attention
 
     @property
     def nseq(self) -> int:
@@ -58,6 +59,21 @@ class Pack:
     @property
     def sum_sq_len(self) -> int:
         return int(np.sum(self.lengths ** 2))
+
+    @property
+    def lengths_k(self) -> np.ndarray:
+        cu = self.cu_seqlens if self.cu_seqlens_k is None else self.cu_seqlens_k
+        return np.diff(cu).astype(np.int64)
+
+    @property
+    def total_tokens_k(self) -> int:
+        cu = self.cu_seqlens if self.cu_seqlens_k is None else self.cu_seqlens_k
+        return int(cu[-1])
+
+    @property
+    def sum_qk(self) -> int:
+        """sum over sequences of Lq * Lk: the score-matrix entries per head (sum L^2 for self-attention)."""
+        return int(np.sum(self.lengths * self.lengths_k))
 
     def f32(self, name: str) -> np.ndarray:
         """The bf16 values of tensor ``name`` widened exactly to float32."""
@@ -118,7 +134,7 @@ def _draw_tensors(seed: int, shape):
     return [_draw_tensor(ss, shape) for ss in np.random.SeedSequence(seed).spawn(4)]
 
 
-WORKLOADS = ("tiny", "uniform", "hetero", "long", "skew")
+WORKLOADS = ("tiny", "uniform", "hetero", "long", "skew", "cross")
 
 DESCRIPTIONS = {
     "tiny": "2 clips (4x8x8=256, 6x8x8=384 tokens), 2 heads x 64",
@@ -126,6 +142,8 @@ DESCRIPTIONS = {
     "hetero": "16 clips drawn from {5x16x16=1,280 p.5; 9x24x32=6,912 p.35; 13x30x52=20,280 p.15}, shuffled, 24 heads x 128",
     "long": "1 clip of 75,600 tokens (21x45x80), 24 heads x 128",
     "skew": "1 clip of 100,800 tokens (28x60x60) + 64 images of 1,024 tokens (1x32x32), shuffled, 40 heads x 128",
+    "cross": "cross-attention: the 16 video clips of the heterogeneous mix as queries, each against 32-256 text "
+             "tokens as keys, 12 heads x 128 (Wan2.1 1.3B)",
 }
 
 
@@ -147,14 +165,28 @@ def workload_shape(name: str, seed: int = 0):
         base = np.array([28 * 60 * 60] + [1 * 32 * 32] * 64)
         lengths = base[rng.permutation(base.shape[0])].tolist()
         H, D = 40, 128
+    elif name == "cross":
+        # Query (video) lengths: the heterogeneous mix's draws; the returned rng then draws the
+        # key (text) lengths (cross_text_lengths).
+        rng, lengths, _, _ = workload_shape("hetero", seed)
+        H, D = 12, 128
     else:
         raise KeyError(f"unknown workload {name!r}; known: {WORKLOADS}")
     return rng, lengths, H, D
 
 
+def cross_text_lengths(rng, nseq: int) -> list:
+    """Text token counts of a cross-attention pack: uniform in [32, 256] (text sequences are
+    short, typically under 256 tokens: Section IV-B footnote)."""
+    return rng.integers(32, 257, size=nseq).tolist()
+
+
 def make_workload(name: str, seed: int = 0, tensors: bool = True) -> Pack:
-    """One of the five named workloads, drawn from ``seed``."""
+    """One of the named workloads, drawn from ``seed``."""
     rng, lengths, H, D = workload_shape(name, seed)
+    if name == "cross":
+        return make_pack_qk(lengths, cross_text_lengths(rng, len(lengths)), H, D, seed=seed, name=name,
+                            tensors=tensors)
     cu = cu_from_lengths(lengths)
     pack = Pack(name=name, cu_seqlens=cu, heads=H, head_dim=D, scale=1.0 / math.sqrt(D))
     if tensors:
@@ -172,8 +204,27 @@ def make_pack(lengths, heads: int, head_dim: int, seed: int = 0, scale: float | 
     return pack
 
 
+def make_pack_qk(lengths_q, lengths_k, heads: int, head_dim: int, seed: int = 0, scale: float | None = None,
+                 name: str = "cross", tensors: bool = True) -> Pack:
+    """A cross-attention pack: sequence s has lengths_q[s] queries and lengths_k[s] keys.
+    q and dout have Tq rows, k and v Tk rows; the four tensors come from the same four
+    streams of the seed as in make_pack (q, k, v, dout)."""
+    cuq, cuk = cu_from_lengths(lengths_q), cu_from_lengths(lengths_k)
+    sc = 1.0 / math.sqrt(head_dim) if scale is None else float(scale)
+    pack = Pack(name=name, cu_seqlens=cuq, heads=heads, head_dim=head_dim, scale=sc, cu_seqlens_k=cuk)
+    if tensors:
+        ss = np.random.SeedSequence(seed).spawn(4)
+        tq, tk = int(cuq[-1]), int(cuk[-1])
+        pack.q = _draw_tensor(ss[0], (tq, heads, head_dim))
+        pack.k = _draw_tensor(ss[1], (tk, heads, head_dim))
+        pack.v = _draw_tensor(ss[2], (tk, heads, head_dim))
+        pack.dout = _draw_tensor(ss[3], (tq, heads, head_dim))
+    return pack
+
+
 def attention_flops(pack: Pack) -> dict:
-    """FLOP conventions for bidirectional attention over the pack (per sequence L^2 work)."""
-    base = pack.heads * pack.head_dim * pack.sum_sq_len
+    """FLOP conventions for bidirectional attention over the pack (per sequence Lq * Lk work;
+    L^2 for self-attention)."""
+    base = pack.heads * pack.head_dim * pack.sum_qk
     return {"fwd": 4 * base, "bwd": 10 * base, "fwd_bwd": 14 * base,
             "no_recompute": 12 * base, "executed": 18 * base}

@@ -28,8 +28,9 @@ def run_hip(pack, dev=None, scale=None):
     from paper_2607_01701_amd import attn_bwd, attn_fwd
     d = dev_inputs(pack) if dev is None else dev
     sc = pack.scale if scale is None else scale
-    out, lse = attn_fwd(d["q"], d["k"], d["v"], pack.cu_seqlens, sc)
-    dq, dk, dv = attn_bwd(d["q"], d["k"], d["v"], out, lse, d["dout"], pack.cu_seqlens, sc)
+    ck = pack.cu_seqlens_k
+    out, lse = attn_fwd(d["q"], d["k"], d["v"], pack.cu_seqlens, sc, cu_seqlens_k=ck)
+    dq, dk, dv = attn_bwd(d["q"], d["k"], d["v"], out, lse, d["dout"], pack.cu_seqlens, sc, cu_seqlens_k=ck)
     torch.cuda.synchronize()
     return {"out": out, "lse": lse, "dq": dq, "dk": dk, "dv": dv}
 
@@ -43,16 +44,19 @@ def rel_err(g, r):
     return float(np.max(np.abs(g - r))) / den if den > 0 else float(np.max(np.abs(g)))
 
 
-def compare_full(g, ref, cu, label=""):
-    """Whole-tensor gate plus a per-clip diagnostic. Returns dict of errors."""
+def compare_full(g, ref, cu, label="", cu_k=None):
+    """Whole-tensor gate plus a per-sequence diagnostic (dk, dv on the key offsets cu_k when
+    given). Returns dict of errors."""
+    cu_k = cu if cu_k is None else cu_k
     errs = {k: rel_err(g[k], ref[k]) for k in ("out", "dq", "dk", "dv")}
     errs["lse"] = float(np.max(np.abs(g["lse"] - ref["lse"]))) if g["lse"].size else 0.0
     worst = {}
     for s in range(len(cu) - 1):
-        a, b = int(cu[s]), int(cu[s + 1])
-        if b == a:
-            continue
         for k in ("out", "dq", "dk", "dv"):
+            c = cu if k in ("out", "dq") else cu_k
+            a, b = int(c[s]), int(c[s + 1])
+            if b == a:
+                continue
             e = rel_err(g[k][a:b], ref[k][a:b])
             worst[k] = max(worst.get(k, 0.0), e)
     log(f"{label} errors {errs} worst-per-clip {worst}")

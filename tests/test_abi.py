@@ -133,3 +133,65 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(_lib, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(ImportError):
         _lib.lib()
+
+
+def fwd_qk(cuq, cuk, heads=2, head_dim=128, scale=0.125, q=A, k=A + 64 * MB, v=A + 128 * MB, out=A + 192 * MB,
+           lse=A + 256 * MB, nseq=None):
+    P = ctypes.POINTER(ctypes.c_int32)
+    cq = None if cuq is None else np.asarray(cuq, dtype=np.int32)
+    ck = None if cuk is None else np.asarray(cuk, dtype=np.int32)
+    n = (cq if cq is not None else ck).shape[0] - 1 if nseq is None else nseq
+    L = _lib.lib()
+    st = L.t2v_attn_fwd_qk(q, k, v, None if cq is None else cq.ctypes.data_as(P),
+                           None if ck is None else ck.ctypes.data_as(P), n, heads, head_dim, scale, out, lse, None)
+    return st, _lib.t2v_last_error(L)
+
+
+@pytest.mark.parametrize("cuq,cuk,kw,msg", [
+    ([0, 5, 9], [0, 0, 3], {}, "has queries but no keys"),
+    ([0, 0, 9], [0, 4, 7], {}, "has keys but no queries"),
+    ([0, 5, 9], [0, 3, 1], {}, "cu_seqlens_k"),
+    ([0, 5, 9], [1, 3, 4], {}, "cu_seqlens_k"),
+    ([0, 5, 9], None, {}, "NULL"),
+    (None, [0, 5, 9], {}, "NULL"),
+    ([0, 5, 9], [0, 2, 3], {"head_dim": 96}, "head_dim"),
+    # out spans Tq = 9 rows of 2 x 128 bf16 (4,608 bytes): it reaches v placed right after it
+    ([0, 5, 9], [0, 2, 3], {"out": A + 192 * MB, "v": A + 192 * MB + 4096}, "overlaps"),
+    # lse spans H * Tq floats = 72 bytes
+    ([0, 5, 9], [0, 2, 3], {"lse": A + 256 * MB, "k": A + 256 * MB + 64}, "overlaps"),
+])
+def test_fwd_qk_validation(cuq, cuk, kw, msg):
+    st, err = fwd_qk(cuq, cuk, **kw)
+    assert st in (INV, UNS), err
+    assert msg in err
+
+
+def test_fwd_qk_sizes_follow_each_stream():
+    """k and v are sized by Tk, not Tq. With Tq = 9 and Tk = 3 (k spans 1,536 bytes), out placed
+    2 KB after k overlaps nothing; lse is then made to overlap out, so validation still stops the
+    call, and the message shows which check fired."""
+    st, err = fwd_qk([0, 5, 9], [0, 2, 3], k=A + 64 * MB, out=A + 64 * MB + 2048, lse=A + 64 * MB + 2048 + 256)
+    assert st == INV
+    assert "input k" not in err and "overlaps output" in err
+
+
+def test_fwd_qk_empty_is_ok():
+    st, _ = fwd_qk([0, 0, 0], [0, 0, 0], q=0, k=0, v=0, out=0, lse=0)
+    assert st == _lib.T2V_OK
+
+
+def test_bwd_qk_validation():
+    P = ctypes.POINTER(ctypes.c_int32)
+    cq = np.asarray([0, 4, 10], dtype=np.int32)
+    ck = np.asarray([0, 0, 6], dtype=np.int32)
+    L = _lib.lib()
+    st = L.t2v_attn_bwd_qk(A, A + 64 * MB, A + 128 * MB, A + 192 * MB, A + 256 * MB, cq.ctypes.data_as(P),
+                           ck.ctypes.data_as(P), 2, 2, 128, 0.125, A + 320 * MB, A + 384 * MB, A + 448 * MB,
+                           A + 512 * MB, A + 576 * MB, None)
+    assert st == INV and "no keys" in _lib.t2v_last_error(L)
+    ck = np.asarray([0, 3, 6], dtype=np.int32)
+    # dk (Tk = 6 rows, 3 KB) aliasing dv
+    st = L.t2v_attn_bwd_qk(A, A + 64 * MB, A + 128 * MB, A + 192 * MB, A + 256 * MB, cq.ctypes.data_as(P),
+                           ck.ctypes.data_as(P), 2, 2, 128, 0.125, A + 320 * MB, A + 384 * MB, A + 448 * MB,
+                           A + 448 * MB + 1024, A + 576 * MB, None)
+    assert st == INV and "overlaps" in _lib.t2v_last_error(L)

@@ -89,8 +89,9 @@ def test_xcd_cost_balance(name):
 
 @pytest.mark.parametrize("name", WORKLOADS)
 def test_workload_item_counts(name):
-    """Item counts of the five workloads at 128-row tiles (hetero at seed 0)."""
-    expect = {"tiny": 10, "uniform": 6144, "hetero": 21960, "long": 14184, "skew": 52000}
+    """Item counts of the workloads at 128-row tiles of the query offsets (hetero and cross at seed 0;
+    cross tiles its 16 video clips over 12 heads)."""
+    expect = {"tiny": 10, "uniform": 6144, "hetero": 21960, "long": 14184, "skew": 52000, "cross": 10980}
     p = make_workload(name, tensors=False)
     items = t2v_build_worklist(p.cu_seqlens, p.heads, 128, ORDER_LONGEST_FIRST)
     assert items.shape[0] == expect[name]
