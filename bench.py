@@ -67,6 +67,10 @@ def parse_args():
                     help="sweep uniform buckets (B clips of S tokens) for three model shapes, fit the attention term "
                          "of the DiT latency model (alpha_2 B S^2 + alpha_1 B S + c0, k = 1) and check it on held-out "
                          "mixed packs; prints a text report")
+    ap.add_argument("--plan", action="store_true",
+                    help="(CPU) plan one training batch of the heterogeneous mix as a cascade DAG on N GPUs with the "
+                         "native genetic-algorithm planner; attention latency from the fitted cost model; compares "
+                         "against static parallel degrees and prints a text report")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain device copy of known size (for HBM counter scaling)")
     ap.add_argument("--ingest-rocpd", nargs=5, metavar=("KT_DB", "FETCH_DB", "WRITE_DB", "COPY_FETCH_DB",
@@ -431,6 +435,80 @@ def cost_model_sweep(steps: int = 4, warmup: int = 2):
     return "\n".join(lines)
 
 
+def plan_batch_report(n_gpus: int = 16, seed: int = 0):
+    """Cascade plan of one batch (paper Section IV-A, Eqs. (1)-(7); Alg. 1) on the CPU.
+
+    Each clip of the heterogeneous mix is three cascades: VAE encode -> DiT forward/backward,
+    and a text encoder -> the same DiT cascade. The DiT's latency at degree k follows Eq. (9):
+    (alpha_1 S + alpha_2 S^2) / k for the attention of 60 layers (HunyuanVideo-13B shape, 24 x 128,
+    coefficients of the MI355X attention cost model in profiles/attn_cost_model_sweep.txt), a
+    linear per-token term of the same size standing in for the rest of the block, and an
+    All-to-All term for k > 1 over xGMI; memory follows Eq. (8). The VAE and text-encoder
+    latencies are linear in tokens. Every constant not measured here is stated below and is
+    an assumption of this synthetic batch, not a measurement.
+    """
+    import numpy as np
+
+    from paper_2607_01701_amd import planner
+    from paper_2607_01701_amd.workload import workload_shape
+
+    lengths = workload_shape("hetero", seed)[1]
+    layers, H, D = 60, 24, 128
+    alpha2 = 4.734197e-08 * 1e-3 * layers        # s per token^2, attention fwd+bwd, all layers (fitted, 24 x 128)
+    alpha1_attn = 1.023822e-05 * 1e-3 * layers   # s per token (fitted)
+    alpha1_rest = 4 * 2 * 3 * (H * D) ** 2 * 12 / 1.0e15 * layers / (H * D)  # MLP+proj GEMMs at 1 PF/s, s/token
+    hidden_bytes = H * D * 2
+    a2a_bw = 7 * 153e9                           # xGMI: 7 links x ~153 GB/s per GPU
+    W = 288e9                                    # bytes per GPU
+    mem_states = 13e9 * 16 / n_gpus + 8e9        # ZeRO-3 sharded model states + workspace (assumption)
+    mem_token = 60 * hidden_bytes * 34           # activation bytes per token across the layers (assumption)
+    K = [k for k in (1, 2, 4, 8) if k <= n_gpus]
+    preds, lat, mem, names = [], [], [], []
+    for i, S in enumerate(lengths):
+        v = len(preds)                            # VAE encode of the clip
+        preds.append([])
+        lat.append([S * 2.0e-6 / k ** 0.9 for k in K])
+        mem.append([20e9 + S * 4.0e5 / k for k in K])
+        names.append(f"vae{i}")
+        t = len(preds)                            # text encoder (short sequence)
+        preds.append([])
+        lat.append([0.02 / k ** 0.5 for k in K])
+        mem.append([10e9] * len(K))
+        names.append(f"txt{i}")
+        preds.append([v, t])                      # DiT forward + backward
+        comp = alpha1_attn * S + alpha2 * S * S + alpha1_rest * S
+        lat.append([comp / k + (0.0 if k == 1 else 4 * layers * 2 * S * hidden_bytes * (k - 1) / k / a2a_bw)
+                    for k in K])
+        mem.append([mem_states + S * mem_token / k for k in K])
+        names.append(f"dit{i}")
+    n = len(preds)
+    t0 = time.perf_counter()
+    deg, starts, T = planner.plan(preds, K, lat, mem, W, n_gpus, population=64, generations=300, seed=seed)
+    t_plan = time.perf_counter() - t0
+    lines = [f"Cascade plan of one batch: the heterogeneous mix (seed {seed}, {len(lengths)} clips) as {n} cascades "
+             f"on N = {n_gpus} GPUs, degrees K = {K} (Section IV-A, Eqs. (1)-(7); Alg. 1).",
+             "Latency inputs: DiT attention from the MI355X cost model (24 x 128, 60 layers: alpha2 = "
+             f"{alpha2:.3e} s/token^2, alpha1 = {alpha1_attn:.3e} s/token); assumed: rest of the block "
+             f"{alpha1_rest:.3e} s/token, All-to-All over 7 x 153 GB/s xGMI, VAE 2e-6 s/token / k^0.9, "
+             "text encoder 0.02 s / k^0.5; memory Eq. (8) with assumed constants, W = 288 GB.",
+             f"GA: population 64, 300 generations, planning time {t_plan:.2f} s (host CPU, one thread).",
+             f"Planned makespan: {T:.2f} s", "", "Static parallel degree for every cascade (list-scheduled, same DAG):"]
+    for k in K:
+        j = K.index(k)
+        if all(mem[c][j] <= W for c in range(n)):
+            _, Tk = planner.list_schedule(preds, [k] * n, [lat[c][j] for c in range(n)], n_gpus)
+            lines.append(f"  k = {k}: {Tk:.2f} s  (the plan is {100 * (1 - T / Tk):.1f}% shorter)")
+        else:
+            lines.append(f"  k = {k}: infeasible (memory)")
+    lines.append("")
+    lines.append("DiT cascades: clip tokens -> planned degree, start, end (s)")
+    for c in range(n):
+        if names[c].startswith("dit"):
+            i = int(names[c][3:])
+            lines.append(f"  {lengths[i]:6d}  k={deg[c]}  {starts[c]:8.2f}  {starts[c] + lat[c][K.index(deg[c])]:8.2f}")
+    return "\n".join(lines)
+
+
 def run_workload(workload, seed, steps, warmup, order=None):
     """Times `steps` fwd+bwd steps of one workload after `warmup` untimed ones; returns the
     bench record (without the CPU baseline) and the pack."""
@@ -573,6 +651,9 @@ def main():
         return
     if args.write_summaries:
         write_summaries(*args.write_summaries[:2])
+        return
+    if args.plan:
+        print(plan_batch_report(), flush=True)
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:

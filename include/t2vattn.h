@@ -140,6 +140,35 @@ int t2v_build_worklist(const int32_t* cu_seqlens, int nseq, int heads, int block
 int t2v_plan_makespan(const int32_t* items, int n_items, int block, int slots,
                       double* makespan_out, double* lower_bound_out);
 
+/* Cascade scheduling (paper Section IV-A, Eqs. (1)-(7)), host-only. Cascades c = 0..n-1
+ * form a DAG given by predecessor lists in CSR form: the direct predecessors of c are
+ * pred_idx[pred_ptr[c] .. pred_ptr[c+1]-1] (pred_ptr[0] = 0, non-decreasing; indices in
+ * 0..n-1, no self-loops; a cycle is T2V_ERR_INVALID_ARG). A schedule gives each cascade a
+ * parallel degree k_c (GPUs) and a launch time s_c >= the end of every predecessor; the
+ * degrees of the cascades running at any time sum to at most n_gpus.
+ *
+ * t2v_list_schedule: for fixed degrees (degree[c] in 1..n_gpus) and latencies (latency[c],
+ * finite, >= 0), the critical-path list schedule: the ready cascade with the longest chain
+ * of latencies from it to the end of the graph goes first, at the earliest time its
+ * predecessors have ended and its GPUs are free for its whole latency. Writes start_out[n]
+ * (host doubles) and the makespan. */
+int t2v_list_schedule(int n_cascades, const int32_t* pred_ptr, const int32_t* pred_idx,
+                      const int32_t* degree, const double* latency, int n_gpus,
+                      double* start_out, double* makespan_out);
+
+/* t2v_plan_cascades: chooses the degrees too (Alg. 1: a genetic algorithm whose fitness is
+ * t2v_list_schedule's makespan). degrees[n_degrees] is the set K (each >= 1); latency and
+ * mem are host doubles [n_cascades][n_degrees]: L_{c,k} and Mem_{c,k}. A degree is feasible
+ * for c when Mem_{c,k} <= mem_cap (W) and k <= n_gpus; a cascade with none is
+ * T2V_ERR_INVALID_ARG. GA hyper-parameters: population >= 2, generations >= 0, mutation
+ * rate in [0, 1], 0 <= elite <= population; seed makes the result reproducible. Writes the
+ * best schedule found: degree_out[n] (the chosen k), start_out[n], makespan_out. */
+int t2v_plan_cascades(int n_cascades, const int32_t* pred_ptr, const int32_t* pred_idx,
+                      int n_degrees, const int32_t* degrees, const double* latency,
+                      const double* mem, double mem_cap, int n_gpus,
+                      int population, int generations, double mutation, int elite, uint64_t seed,
+                      int32_t* degree_out, double* start_out, double* makespan_out);
+
 /* Per-kernel timing, for measurement. While enabled, every kernel launch is bracketed by
  * two HIP events recorded on the launch stream. t2v_kernel_times waits for the recorded
  * events, returns the summed elapsed milliseconds and the launch count of each kernel since

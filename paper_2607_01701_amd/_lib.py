@@ -29,9 +29,10 @@ ORDER_LONGEST_FIRST = 1
 # Symbols declared in include/t2vattn.h.
 EXPORTS = ("t2v_attn_fwd", "t2v_attn_bwd", "t2v_attn_fwd_qk", "t2v_attn_bwd_qk", "t2v_last_error",
            "t2v_release_cache", "t2v_build_worklist", "t2v_plan_makespan", "t2v_timing_enable", "t2v_kernel_times",
-           "t2v_version")
+           "t2v_version", "t2v_list_schedule", "t2v_plan_cascades")
 KERNEL_SLOTS = ("fwd", "bwd_pre", "bwd_dkdv", "bwd_dq")
-HOST_EXPORTS = ("t2v_last_error", "t2v_build_worklist", "t2v_plan_makespan", "t2v_version")
+HOST_EXPORTS = ("t2v_last_error", "t2v_build_worklist", "t2v_plan_makespan", "t2v_version", "t2v_list_schedule",
+                "t2v_plan_cascades")
 
 _vp = ctypes.c_void_p
 _i32p = ctypes.POINTER(ctypes.c_int32)
@@ -55,6 +56,13 @@ def _declare(lib, full: bool):
     lib.t2v_plan_makespan.restype = ctypes.c_int
     lib.t2v_plan_makespan.argtypes = [_i32p, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                       ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
+    _dp = ctypes.POINTER(ctypes.c_double)
+    lib.t2v_list_schedule.restype = ctypes.c_int
+    lib.t2v_list_schedule.argtypes = [ctypes.c_int, _i32p, _i32p, _i32p, _dp, ctypes.c_int, _dp, _dp]
+    lib.t2v_plan_cascades.restype = ctypes.c_int
+    lib.t2v_plan_cascades.argtypes = [ctypes.c_int, _i32p, _i32p, ctypes.c_int, _i32p, _dp, _dp, ctypes.c_double,
+                                      ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_double, ctypes.c_int,
+                                      ctypes.c_uint64, _i32p, _dp, _dp]
     if full:
         lib.t2v_attn_fwd.restype = ctypes.c_int
         lib.t2v_attn_fwd.argtypes = [_vp, _vp, _vp, _i32p, ctypes.c_int, ctypes.c_int, ctypes.c_int,
