@@ -26,26 +26,32 @@ if ROOT not in sys.path:
 METRIC = "varlen attention fwd+bwd TFLOP/s and % of bf16 MFMA peak, 1×MI355X"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+# What decides the attention kernels' code and launches: device sources, the launch code, the
+# tile scheduler, and the HIP compile flags (the planner and other host-only code are left out).
 KERNEL_SOURCES = ("paper_2607_01701_amd/csrc/t2v_fwd.hip", "paper_2607_01701_amd/csrc/t2v_bwd_pre.hip",
                   "paper_2607_01701_amd/csrc/t2v_bwd_dkdv.hip", "paper_2607_01701_amd/csrc/t2v_bwd_dq.hip",
                   "paper_2607_01701_amd/csrc/t2v_kernel_common.hpp", "paper_2607_01701_amd/csrc/t2v_device.hpp",
-                  "paper_2607_01701_amd/build.py")
+                  "paper_2607_01701_amd/csrc/t2v_kernels.h", "paper_2607_01701_amd/csrc/t2v_api.hip",
+                  "paper_2607_01701_amd/csrc/t2v_host.cpp", "paper_2607_01701_amd/csrc/t2v_host.h")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 
 
 def kernel_source_hash() -> str:
-    """Hash of the kernel sources and build flags; C++ comments and blank lines are left out,
-    so comment edits keep profiles taken on the same code valid."""
+    """Hash of the kernel sources and HIP build flags; C++ comments and blank lines are left
+    out, so comment edits keep profiles taken on the same code valid."""
     import re
+
+    from paper_2607_01701_amd import build as _build
     h = hashlib.sha256()
     for rel in KERNEL_SOURCES:
         with open(os.path.join(ROOT, rel), encoding="utf-8") as f:
             text = f.read()
-        if rel.endswith((".hip", ".hpp")):
-            text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-            text = re.sub(r"//[^\n]*", "", text)
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", "", text)
         text = "\n".join(line.rstrip() for line in text.splitlines() if line.strip())
         h.update(text.encode())
+    flags = [f.replace(_build.ROOT, "<root>") for f in _build.HIP_FLAGS]
+    h.update(json.dumps([flags, _build.SCHED], sort_keys=True).encode())
     return h.hexdigest()[:16]
 
 
