@@ -83,6 +83,8 @@ def parse_args():
                                                         "COPY_WRITE_DB"),
                     help="summarise rocprofv3 databases (kernel trace, FETCH_SIZE and WRITE_SIZE of this bench and "
                          "of --copy-calibration) into profiles/; runs on the CPU")
+    ap.add_argument("--ingest-mfma", metavar="PMC_DB",
+                    help="summarise a rocprofv3 MfmaUtil / MfmaFlopsBF16 counter pass into profiles/; runs on the CPU")
     return ap.parse_args()
 
 
@@ -153,8 +155,32 @@ def cpu_baseline(pack, budget_s: float = 15.0):
                 break
     return {"value": flops / t_used * 1e-12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
             "seconds": round(t_used, 3),
+            "gflops_strict_no_recompute": round(flops * 12.0 / 14.0 / t_used * 1e-9, 2),
+            "host": host_info(),
             "sample": f"{len(done)} (clip query tokens, head) pairs of this workload {done}; float64 numpy oracle "
                       f"fwd+bwd, counted at the same 14*D*Lq*Lk per pair"}
+
+
+def host_info() -> dict:
+    """CPU model, logical CPU count and BLAS library of the host the oracle runs on."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = None
+    try:
+        from threadpoolctl import threadpool_info
+        b = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if b:
+            blas = f"{b[0].get('internal_api')} {b[0].get('version')} ({b[0].get('num_threads')} threads)"
+    except Exception:  # pragma: no cover
+        pass
+    return {"cpu_model": model, "nproc": os.cpu_count(), "blas": blas}
 
 
 def copy_calibration():
@@ -228,6 +254,62 @@ def ingest_rocpd(kt_db, fetch_db, write_db, copy_fetch_db, copy_write_db, worklo
     os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
     with open(TRAFFIC_FILE, "w") as f:
         json.dump(rec, f, indent=1, sort_keys=True)
+    print("\n".join(lines))
+
+
+MFMA_CMD = ("rocprofv3 --pmc MfmaUtil MfmaFlopsBF16 SQ_INSTS_MFMA -d gpurun_out/pmc_mfma -o m -- "
+            "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline")
+
+
+def ingest_mfma(pmc_db, workload):
+    """MFMA utilisation per kernel from a rocprofv3 counter pass (derived metrics MfmaUtil =
+    MFMA-busy cycles / (GPU-active cycles x SIMDs), MfmaFlopsBF16 = bf16 MFMA ops x 512);
+    durations from profiles/hbm_traffic.json (same kernel sources). Writes the text summary
+    profiles/attn_fwd_<workload>_mfma_counters.txt."""
+    import sqlite3
+
+    from paper_2607_01701_amd.workload import DESCRIPTIONS, workload_shape
+
+    _, lengths, H, D = workload_shape(workload)
+    ssq = int(sum(int(x) * int(x) for x in lengths))
+    kf = kernel_flops(H, D, ssq)
+    with open(TRAFFIC_FILE) as f:
+        t = json.load(f)
+    if t["kernel_source_hash"] != kernel_source_hash() or t.get("workload") != workload:
+        raise SystemExit("profiles/hbm_traffic.json comes from other kernel sources or another workload")
+    c = sqlite3.connect(pmc_db)
+    rows = c.execute("select kernel_name, counter_name, count(*), avg(value) from counters_collection "
+                     "group by kernel_name, counter_name").fetchall()
+    c.close()
+    by = {}
+    for name, cname, n, avg in rows:
+        slot = _slot(name)
+        if slot:
+            by.setdefault(slot, {})[cname] = (avg, n)
+    lines = [f"rocprofv3 MFMA counters: attention kernels, {workload} workload ({DESCRIPTIONS[workload]})",
+             f"Kernel source hash (bench.py kernel_source_hash): {kernel_source_hash()}", "",
+             "Commands (repo root, GPU box):", "  " + MFMA_CMD,
+             f"  python3 bench.py --ingest-mfma gpurun_out/pmc_mfma/m_results.db --workload {workload}",
+             "Durations: kernel-trace averages of the same sources (profiles/hbm_traffic.json).", "",
+             f"{'kernel':10s} {'MfmaUtil %':>10s} {'MFMA flops/launch':>18s} {'algorithmic':>12s} {'ratio':>6s} "
+             f"{'trace ms':>9s} {'counter TF/s':>12s} {'% of 2.5 PF':>11s}"]
+    for slot in ("bwd_dkdv", "bwd_dq", "fwd"):
+        d = by.get(slot, {})
+        util = d.get("MfmaUtil", (float("nan"), 0))[0]
+        fl = d.get("MfmaFlopsBF16", (float("nan"), 0))[0]
+        ms = t["kernels"][slot]["trace_avg_ms"]
+        tf = fl / (ms * 1e-3) * 1e-12
+        lines.append(f"{slot:10s} {util:10.1f} {fl:18.4e} {kf[slot]:12.4e} {fl / kf[slot]:6.3f} {ms:9.3f} "
+                     f"{tf:12.0f} {100 * tf / PEAK_BF16_TFLOPS:10.1f}%")
+    lines += ["", "MfmaUtil is the share of SIMD cycles with the matrix unit busy at the clock the chip ran; "
+              "'% of 2.5 PF' is the counter-measured MFMA rate against the published bf16 dense peak "
+              "(which assumes the 2.4 GHz peak clock).",
+              "Algorithmic executed MFMA work per launch: fwd 4, dK/dV 8, dQ 6 x H*D*sum(L^2) = "
+              f"{H}*{D}*{ssq:,}; ratio = counter flops / algorithmic (1.000 means no MFMA work beyond "
+              "the design's products, masked tails included)."]
+    out = os.path.join(ROOT, "profiles", f"attn_fwd_bwd_{workload}_mfma_counters.txt")
+    with open(out, "w") as f:
+        f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
 
 
@@ -515,6 +597,25 @@ def plan_batch_report(n_gpus: int = 16, seed: int = 0):
     return "\n".join(lines)
 
 
+def mfma_probe(blocks: int = 2048, iters: int = 40000) -> dict:
+    """The library's MFMA throughput probe: bf16 dense TFLOP/s and shader clock this GPU
+    sustains under a pure MFMA load (context for the attention kernels' rates)."""
+    import torch
+
+    from paper_2607_01701_amd import _lib
+
+    _lib.lib()
+    rec = torch.zeros(3 * blocks, dtype=torch.int64, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    _lib.t2v_probe_mfma_peak(rec.data_ptr(), blocks, 2000, stream)  # warm-up
+    r = _lib.t2v_probe_mfma_peak(rec.data_ptr(), blocks, iters, stream)
+    print(f"[bench] MFMA probe: {r['tflops']:.0f} TFLOP/s at {r['ghz']:.2f} GHz", file=sys.stderr, flush=True)
+    return {"tflops": round(r["tflops"], 1), "ghz": round(r["ghz"], 3), "ms": round(r["ms"], 3),
+            "frac_of_spec_peak": round(r["tflops"] / PEAK_BF16_TFLOPS, 4),
+            "kernel": "4 waves x 4 independent v_mfma_f32_32x32x16_bf16 chains per workgroup, "
+                      f"{blocks} workgroups x {iters} rounds"}
+
+
 def run_workload(workload, seed, steps, warmup, order=None):
     """Times `steps` fwd+bwd steps of one workload after `warmup` untimed ones; returns the
     bench record (without the CPU baseline) and the pack."""
@@ -550,7 +651,7 @@ def run_workload(workload, seed, steps, warmup, order=None):
     sh = stream.cuda_stream
     cup = cu.ctypes.data_as(_lib._i32p)
 
-    def step():
+    def step(mid=None):
         if cross:
             st = L.t2v_attn_fwd_qk(q.data_ptr(), k.data_ptr(), v.data_ptr(), cup, cukp, nseq, H, D, pack.scale,
                                    out.data_ptr(), lse.data_ptr(), sh)
@@ -559,6 +660,8 @@ def run_workload(workload, seed, steps, warmup, order=None):
                                 out.data_ptr(), lse.data_ptr(), sh)
         if st:
             raise _lib.T2VError(st, _lib.t2v_last_error())
+        if mid is not None:
+            mid.record(stream)
         if cross:
             st = L.t2v_attn_bwd_qk(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(), cup, cukp,
                                    nseq, H, D, pack.scale, g.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
@@ -577,16 +680,22 @@ def run_workload(workload, seed, steps, warmup, order=None):
 
     _lib.t2v_timing_enable(True)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # Per step: events before the forward, between forward and backward, after the backward.
+    marks = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
     torch.cuda.synchronize()
     e0.record(stream)
-    for _ in range(steps):
-        step()
+    for i in range(steps):
+        marks[i][0].record(stream)
+        step(marks[i][1])
+        marks[i][2].record(stream)
     e1.record(stream)
     torch.cuda.synchronize()
     ktimes = _lib.t2v_kernel_times()
     _lib.t2v_timing_enable(False)
     ms_step = e0.elapsed_time(e1) / steps
     print(f"[bench] timed {steps} steps: {ms_step:.3f} ms/step", file=sys.stderr, flush=True)
+    per = {"fwd": [m[0].elapsed_time(m[1]) for m in marks], "bwd": [m[1].elapsed_time(m[2]) for m in marks],
+           "fwd_bwd": [m[0].elapsed_time(m[2]) for m in marks]}
 
     fl = attention_flops(pack)
     tflops = fl["fwd_bwd"] / (ms_step * 1e-3) * 1e-12
@@ -615,6 +724,19 @@ def run_workload(workload, seed, steps, warmup, order=None):
                                      "bwd_dq": "6*H*D*sum(L^2)"}[dominant]}
     fwd_ms = avg["fwd"]
     bwd_ms = sum(avg[n] for n in ("bwd_pre", "bwd_dkdv", "bwd_dq") if avg.get(n))
+    conv = {"fwd": fl["fwd"], "bwd": fl["bwd"], "fwd_bwd": fl["fwd_bwd"]}
+    timing = {}
+    for name, xs in per.items():
+        med = float(np.median(xs))
+        timing[name] = {"median_ms": round(med, 4), "mean_ms": round(float(np.mean(xs)), 4),
+                        "min_ms": round(float(np.min(xs)), 4),
+                        "tflops_at_median": round(conv[name] / (med * 1e-3) * 1e-12, 2)}
+    flops = {"counted_fwd_bwd": fl["fwd_bwd"], "strict_no_recompute": fl["no_recompute"],
+             "executed_mfma": fl["executed"],
+             "tflops_strict_no_recompute": round(fl["no_recompute"] / (ms_step * 1e-3) * 1e-12, 2),
+             "tflops_executed_mfma": round(fl["executed"] / (ms_step * 1e-3) * 1e-12, 2),
+             "exp2_fwd": H * pack.sum_qk, "exp2_bwd": 2 * H * pack.sum_qk,
+             "note": "counted 14, strict no-recompute 12, executed 18 (fwd 4 + dK/dV 8 + dQ 6) x H*D*sum(Lq*Lk)"}
     res = {
         "metric": METRIC,
         "value": round(tflops, 2),
@@ -636,6 +758,8 @@ def run_workload(workload, seed, steps, warmup, order=None):
         "frac_of_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
         "fwd_tflops": round(fl["fwd"] / (fwd_ms * 1e-3) * 1e-12, 2),
         "bwd_tflops": round(fl["bwd"] / (bwd_ms * 1e-3) * 1e-12, 2),
+        "timing": timing,
+        "flops": flops,
         "kernels": kernels,
         "roofline": roofline,
         "kernel_source_hash": kernel_source_hash(),
@@ -654,6 +778,9 @@ def main():
     args = parse_args()
     if args.ingest_rocpd:
         ingest_rocpd(*args.ingest_rocpd, workload=args.workload)
+        return
+    if args.ingest_mfma:
+        ingest_mfma(args.ingest_mfma, workload=args.workload)
         return
     if args.write_summaries:
         write_summaries(*args.write_summaries[:2])
@@ -688,6 +815,8 @@ def main():
             print(json.dumps(res), flush=True)
         return
     res, pack = run_workload(args.workload, args.seed, args.steps, args.warmup)
+    res["mfma_probe"] = mfma_probe()
+    res["roofline"]["frac_of_probe"] = round(res["roofline"]["achieved"] / res["mfma_probe"]["tflops"], 4)
     if not args.no_cpu_baseline:
         print("[bench] timing the float64 oracle on a bounded sample", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(pack)

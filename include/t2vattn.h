@@ -179,6 +179,21 @@ int t2v_plan_cascades(int n_cascades, const int32_t* pred_ptr, const int32_t* pr
 int t2v_timing_enable(int on);
 int t2v_kernel_times(double* ms_out, int* counts_out);
 
+/* MFMA throughput probe, for measurement context only (not part of the attention path).
+ * Launches `blocks` workgroups of four waves; each wave runs four independent chains of
+ * `iters` v_mfma_f32_32x32x16_bf16 with no memory traffic, on `stream`, and waits for it.
+ *   rec         device unsigned long long[3 * blocks], caller-owned; per workgroup: shader
+ *               clock ticks, wall-clock ticks, a checksum word (overwritten)
+ *   blocks      1 .. 2^20;  iters 1 .. 2^24
+ *   ms_out      elapsed milliseconds between HIP events around the launch
+ *   tflops_out  bf16 dense TFLOP/s achieved (2 * 32 * 32 * 16 flops per MFMA)
+ *   ghz_out     average shader clock over the run (clock ticks / wall-clock ticks times the
+ *               device's wall-clock rate)
+ * NULL pointers or sizes out of range: T2V_ERR_INVALID_ARG before any launch; HIP failures:
+ * T2V_ERR_HIP. */
+int t2v_probe_mfma_peak(unsigned long long* rec, int blocks, int iters, void* stream, double* ms_out,
+                        double* tflops_out, double* ghz_out);
+
 /* Library version, for diagnostics. */
 const char* t2v_version(void);
 

@@ -29,7 +29,7 @@ ORDER_LONGEST_FIRST = 1
 # Symbols declared in include/t2vattn.h.
 EXPORTS = ("t2v_attn_fwd", "t2v_attn_bwd", "t2v_attn_fwd_qk", "t2v_attn_bwd_qk", "t2v_last_error",
            "t2v_release_cache", "t2v_build_worklist", "t2v_plan_makespan", "t2v_timing_enable", "t2v_kernel_times",
-           "t2v_version", "t2v_list_schedule", "t2v_plan_cascades")
+           "t2v_version", "t2v_list_schedule", "t2v_plan_cascades", "t2v_probe_mfma_peak")
 KERNEL_SLOTS = ("fwd", "bwd_pre", "bwd_dkdv", "bwd_dq")
 HOST_EXPORTS = ("t2v_last_error", "t2v_build_worklist", "t2v_plan_makespan", "t2v_version", "t2v_list_schedule",
                 "t2v_plan_cascades")
@@ -82,6 +82,8 @@ def _declare(lib, full: bool):
         lib.t2v_timing_enable.argtypes = [ctypes.c_int]
         lib.t2v_kernel_times.restype = ctypes.c_int
         lib.t2v_kernel_times.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int)]
+        lib.t2v_probe_mfma_peak.restype = ctypes.c_int
+        lib.t2v_probe_mfma_peak.argtypes = [_vp, ctypes.c_int, ctypes.c_int, _vp, _dp, _dp, _dp]
     return lib
 
 
@@ -170,6 +172,14 @@ def t2v_kernel_times() -> dict:
     n = (ctypes.c_int * 4)()
     _check(lib(), lib().t2v_kernel_times(ms, n))
     return {name: (ms[i], n[i]) for i, name in enumerate(KERNEL_SLOTS)}
+
+
+def t2v_probe_mfma_peak(rec, blocks: int, iters: int, stream) -> dict:
+    """MFMA throughput probe (measurement context); rec: device address of 3 * blocks uint64."""
+    ms, tf, ghz = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+    _check(lib(), lib().t2v_probe_mfma_peak(rec, int(blocks), int(iters), stream, ctypes.byref(ms),
+                                            ctypes.byref(tf), ctypes.byref(ghz)))
+    return {"ms": ms.value, "tflops": tf.value, "ghz": ghz.value}
 
 
 def t2v_version(L=None) -> str:

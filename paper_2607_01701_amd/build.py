@@ -21,7 +21,8 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libt2vattn.so")
 HOST_LIB = os.path.join(PKG, "libt2vattn_host.so")
 
-HIP_SOURCES = ["t2v_fwd.hip", "t2v_bwd_pre.hip", "t2v_bwd_dkdv.hip", "t2v_bwd_dq.hip", "t2v_api.hip"]
+HIP_SOURCES = ["t2v_fwd.hip", "t2v_bwd_pre.hip", "t2v_bwd_dkdv.hip", "t2v_bwd_dq.hip", "t2v_api.hip",
+               "t2v_probe.hip"]
 HOST_SOURCES = ["t2v_host.cpp", "t2v_plan.cpp"]
 
 ARCH = os.environ.get("T2V_OFFLOAD_ARCH", "gfx950")

@@ -195,3 +195,17 @@ def test_bwd_qk_validation():
                            ck.ctypes.data_as(P), 2, 2, 128, 0.125, A + 320 * MB, A + 384 * MB, A + 448 * MB,
                            A + 448 * MB + 1024, A + 576 * MB, None)
     assert st == INV and "overlaps" in _lib.t2v_last_error(L)
+
+
+def test_mfma_probe_validation():
+    """The MFMA probe rejects NULL buffers and out-of-range sizes before touching the GPU."""
+    L = _lib.lib()
+    d = ctypes.c_double()
+    ref = ctypes.byref(d)
+    assert L.t2v_probe_mfma_peak(None, 4, 10, None, ref, ref, ref) == _lib.T2V_ERR_INVALID_ARG
+    assert "NULL" in _lib.t2v_last_error(L)
+    fake = ctypes.c_void_p(4096)  # never dereferenced: the sizes are rejected first
+    for blocks, iters in ((0, 10), (4, 0), (1 << 21, 10), (4, 1 << 25)):
+        assert L.t2v_probe_mfma_peak(fake, blocks, iters, None, ref, ref, ref) == _lib.T2V_ERR_INVALID_ARG
+        assert "blocks must be" in _lib.t2v_last_error(L)
+    assert L.t2v_probe_mfma_peak(fake, 4, 10, None, None, ref, ref) == _lib.T2V_ERR_INVALID_ARG
