@@ -289,7 +289,32 @@ def check_brute_force(mod):
     return all(rel(r[key], b[key]) < 1e-12 for key in ("out", "dq", "dk", "dv", "lse"))
 
 
+def check_dominant_key(mod):
+    """P16: one key's score exceeds every other by 1,000 (natural units): the softmax is
+    exactly one-hot in float64, so out = that key's value row, lse = its score, dq = dk = 0
+    (up to rounding), and dv is the summed dout on that key, zero elsewhere. Scores this large also overflow
+    any exponential taken without subtracting the row maximum."""
+    L, D, star = 6, 8, 3
+    cu, q, k, v, do = rand_pack([L], 1, D, 16)
+    q[:, 0, :] = 0.0
+    q[:, 0, 0] = 50.0
+    k[:, 0, 0] = 0.0  # other dimensions keep their noise, orthogonal to every query
+    k[star, 0, 0] = 40.0
+    sc = 0.5  # scores: 1,000 on the dominant key, exactly 0 elsewhere
+    r = mod.attention(q, k, v, do, cu, sc)
+    ok = np.array_equal(r["out"][:, 0], np.broadcast_to(v[star, 0], (L, D)))
+    ok &= np.array_equal(r["lse"][0], np.full(L, 1000.0))
+    # dS = P (dP - Delta) vanishes: on the dominant key dP and Delta are the same dot product
+    # (rounded along two summation paths), elsewhere P = 0.
+    ok &= np.all(np.abs(r["dq"]) < 1e-12) and np.all(np.abs(r["dk"]) < 1e-12)
+    dv = np.zeros((L, D))
+    dv[star] = do[:, 0].sum(axis=0)
+    ok &= np.allclose(r["dv"][:, 0], dv, rtol=0, atol=1e-13)
+    return bool(ok)
+
+
 PINS = {
+    "P16_dominant_key": check_dominant_key,
     "P1_len1": check_len1,
     "P2_equal_v": check_equal_v,
     "P3_equal_k": check_equal_k,
@@ -395,6 +420,7 @@ MUTANTS = {
     "dQ_uses_V": ("dQ[r0:r1] = scale * (dS @ K)", "dQ[r0:r1] = scale * (dS @ V)"),
     "dK_uses_K": ("dK += scale * (dS.T @ Qb)", "dK += scale * (dS.T @ K[r0:r1])"),
     "dP_uses_K": ("dP = dOb @ V.T", "dP = dOb @ K.T"),
+    "softmax_no_max_shift": ("E = np.exp(S - m[:, None])", "E = np.exp(S)"),
 }
 
 
@@ -414,8 +440,9 @@ def test_mutants_are_caught(name):
         if pin in ("P12_finite_differences", "P13_brute_force"):
             continue  # the cheaper pins must already catch every mutant
         try:
-            if not fn(mod):
-                failing.append(pin)
+            with np.errstate(over="ignore", invalid="ignore", divide="ignore"):  # mutants may overflow
+                if not fn(mod):
+                    failing.append(pin)
         except Exception:  # a shape error is also a detection
             failing.append(pin)
     assert failing, f"mutant {name} passed every pin"
