@@ -257,7 +257,9 @@ def ingest_rocpd(kt_db, fetch_db, write_db, copy_fetch_db, copy_write_db, worklo
     print("\n".join(lines))
 
 
-MFMA_CMD = ("rocprofv3 --pmc MfmaUtil MfmaFlopsBF16 SQ_INSTS_MFMA -d gpurun_out/pmc_mfma -o m -- "
+def mfma_cmd(out):
+    """The counter pass summarised by --ingest-mfma, writing under directory `out`."""
+    return (f"rocprofv3 --pmc MfmaUtil MfmaFlopsBF16 SQ_INSTS_MFMA -d {out}/pmc_mfma -o m -- "
             "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline")
 
 
@@ -288,8 +290,8 @@ def ingest_mfma(pmc_db, workload):
             by.setdefault(slot, {})[cname] = (avg, n)
     lines = [f"rocprofv3 MFMA counters: attention kernels, {workload} workload ({DESCRIPTIONS[workload]})",
              f"Kernel source hash (bench.py kernel_source_hash): {kernel_source_hash()}", "",
-             "Commands (repo root, GPU box):", "  " + MFMA_CMD,
-             f"  python3 bench.py --ingest-mfma gpurun_out/pmc_mfma/m_results.db --workload {workload}",
+             "Commands (repo root, on the GPU):", "  " + mfma_cmd(os.path.dirname(os.path.dirname(pmc_db)) or "."),
+             f"  python3 bench.py --ingest-mfma {pmc_db} --workload {workload}",
              "Durations: kernel-trace averages of the same sources (profiles/hbm_traffic.json).", "",
              f"{'kernel':10s} {'MfmaUtil %':>10s} {'MFMA flops/launch':>18s} {'algorithmic':>12s} {'ratio':>6s} "
              f"{'trace ms':>9s} {'counter TF/s':>12s} {'% of 2.5 PF':>11s}"]
@@ -313,17 +315,20 @@ def ingest_mfma(pmc_db, workload):
     print("\n".join(lines))
 
 
-PROFILE_CMDS = """Commands (repo root, GPU box; rocprofv3 writes rocpd SQLite files):
-  rocprofv3 --kernel-trace --stats -d gpurun_out/prof_kt -o kt -- python3 bench.py --steps 20 --warmup 5 --no-cpu-baseline
-  rocprofv3 --pmc FETCH_SIZE -d gpurun_out/pmc_fetch -o f -- python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline
-  rocprofv3 --pmc WRITE_SIZE -d gpurun_out/pmc_write -o w -- python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline
-  rocprofv3 --pmc FETCH_SIZE -d gpurun_out/pmc_copy_fetch -o cf -- python3 bench.py --copy-calibration
-  rocprofv3 --pmc WRITE_SIZE -d gpurun_out/pmc_copy_write -o cw -- python3 bench.py --copy-calibration
-  python3 bench.py --steps 20 --warmup 5 > gpurun_out/bench_hetero.json
+def profile_cmds(out):
+    """The kernel-trace and HBM-counter passes summarised by --ingest-rocpd and
+    --write-summaries, writing under directory `out`."""
+    return f"""Commands (repo root, on the GPU; rocprofv3 writes rocpd SQLite files):
+  rocprofv3 --kernel-trace --stats -d {out}/prof_kt -o kt -- python3 bench.py --steps 20 --warmup 5 --no-cpu-baseline
+  rocprofv3 --pmc FETCH_SIZE -d {out}/pmc_fetch -o f -- python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline
+  rocprofv3 --pmc WRITE_SIZE -d {out}/pmc_write -o w -- python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline
+  rocprofv3 --pmc FETCH_SIZE -d {out}/pmc_copy_fetch -o cf -- python3 bench.py --copy-calibration
+  rocprofv3 --pmc WRITE_SIZE -d {out}/pmc_copy_write -o cw -- python3 bench.py --copy-calibration
+  python3 bench.py --steps 20 --warmup 5 > {out}/bench_hetero.json
 Summarised with:
-  python3 bench.py --ingest-rocpd gpurun_out/prof_kt/kt_results.db gpurun_out/pmc_fetch/f_results.db \\
-      gpurun_out/pmc_write/w_results.db gpurun_out/pmc_copy_fetch/cf_results.db gpurun_out/pmc_copy_write/cw_results.db
-  python3 bench.py --write-summaries gpurun_out/bench_hetero.json gpurun_out/sweep.jsonl
+  python3 bench.py --ingest-rocpd {out}/prof_kt/kt_results.db {out}/pmc_fetch/f_results.db \\
+      {out}/pmc_write/w_results.db {out}/pmc_copy_fetch/cf_results.db {out}/pmc_copy_write/cw_results.db
+  python3 bench.py --write-summaries {out}/bench_hetero.json {out}/sweep.jsonl
 """
 
 
@@ -342,7 +347,8 @@ def write_summaries(bench_json, sweep_jsonl=None):
     alg = {"fwd": 4 * hds, "bwd_dkdv": 8 * hds, "bwd_dq": 6 * hds}
     head = ("attention forward + backward kernels, heterogeneous mix workload\n"
             "(16 clips: 6x1,280 + 7x6,912 + 3x20,280 tokens, 24 heads x 128, bf16), one MI355X.\n"
-            f"Kernel source hash (bench.py kernel_source_hash): {t['kernel_source_hash']}\n\n" + PROFILE_CMDS + "\n")
+            f"Kernel source hash (bench.py kernel_source_hash): {t['kernel_source_hash']}\n\n"
+            + profile_cmds(os.path.dirname(bench_json) or ".") + "\n")
     order = ("bwd_dkdv", "bwd_dq", "fwd", "bwd_pre")
     lines = ["rocprofv3 kernel trace: " + head, "kernel-trace averages (ms per launch):"]
     lines += [f"  {n:10s} {k[n]['trace_avg_ms']:10.4f}" for n in order]
@@ -383,8 +389,8 @@ def write_summaries(bench_json, sweep_jsonl=None):
             rows = [json.loads(x) for x in f if x.strip()]
         out = ["bench.py --sweep: every workload, fwd + bwd, one MI355X, bf16 in / fp32 accumulate, synthetic "
                "N(0,1) inputs.", f"Kernel source hash (bench.py kernel_source_hash): {rows[0]['kernel_source_hash']}",
-               "", "Command (repo root, GPU box):", "  python3 bench.py --sweep > gpurun_out/sweep.jsonl",
-               "  python3 bench.py --write-summaries gpurun_out/bench_hetero.json gpurun_out/sweep.jsonl",
+               "", "Command (repo root, on the GPU):", f"  python3 bench.py --sweep > {sweep_jsonl}",
+               f"  python3 bench.py --write-summaries {bench_json} {sweep_jsonl}",
                "(one JSON line per run; warmup = min(10, steps / 2); HIP events on the launch stream)", "",
                "FLOP convention: fwd 4*H*D*sum(L^2), bwd 10*H*D*sum(L^2), step 14*H*D*sum(L^2); % of the "
                "2.5 PFLOP/s bf16 dense peak.", "",
