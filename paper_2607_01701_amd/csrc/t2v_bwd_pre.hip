@@ -12,30 +12,53 @@ namespace {
 // ndelta[h, t] = -sum_d dO[t, h, d] O[t, h, d]  and  lse2[h, t] = lse[h, t] * log2(e). Delta is
 // stored negated because the dK/dV kernel starts its dP accumulator from it (dP - Delta
 // then costs no subtraction) and the dQ kernel adds it.
+//
+// A workgroup owns one head and kPreTokens consecutive tokens: D / 8 lanes read one
+// (token, head) row of O and dO (16 bytes each per lane, the row contiguous), the row sums
+// go through LDS, and the [H, T] outputs leave as contiguous runs of kPreTokens floats (the
+// lse reads likewise), rather than as 4-byte accesses T floats apart.
+constexpr int kPreTokens = 64;
+
 template <int D>
 __global__ __launch_bounds__(kThreads) void attn_bwd_pre_kernel(const bf16* __restrict__ out,
                                                                  const bf16* __restrict__ dout,
-                                                                 const float* __restrict__ lse, int64_t rows,
-                                                                 int H, int64_t T, float* __restrict__ ndelta,
+                                                                 const float* __restrict__ lse, int H,
+                                                                 int64_t T, float* __restrict__ ndelta,
                                                                  float* __restrict__ lse2) {
-  constexpr int LPR = D / 8;            // lanes per (token, head) row
-  constexpr int RPB = kThreads / LPR;   // rows per workgroup step
+  constexpr int LPR = D / 8;                 // lanes per (token, head) row
+  constexpr int RPI = kThreads / LPR;        // rows per pass of the workgroup
+  constexpr int NPASS = kPreTokens / RPI;    // passes per tile
+  static_assert(kPreTokens % RPI == 0 && kPreTokens <= kThreads, "whole passes; one store lane per token");
+  __shared__ float sres[kPreTokens];
+  const int64_t ntb = (T + kPreTokens - 1) / kPreTokens;  // token blocks per head
+  const int64_t h = static_cast<int64_t>(blockIdx.x) / ntb;
+  const int64_t t0 = (static_cast<int64_t>(blockIdx.x) - h * ntb) * kPreTokens;
   const int sub = threadIdx.x % LPR;
-  for (int64_t row = static_cast<int64_t>(blockIdx.x) * RPB + threadIdx.x / LPR; row < rows;
-       row += static_cast<int64_t>(gridDim.x) * RPB) {
-    const bf16x8 a = *reinterpret_cast<const bf16x8*>(out + row * D + sub * 8);
-    const bf16x8 g = *reinterpret_cast<const bf16x8*>(dout + row * D + sub * 8);
+  const int r = threadIdx.x / LPR;
+  const int64_t rs = static_cast<int64_t>(H) * D;
+  bf16x8 a[NPASS], g[NPASS];
+#pragma unroll
+  for (int i = 0; i < NPASS; ++i) {
+    const int64_t t = t0 + i * RPI + r;
+    const bool ok = t < T;
+    const int64_t off = (ok ? t : 0) * rs + h * D + sub * 8;
+    a[i] = load8(out + off, ok);
+    g[i] = load8(dout + off, ok);
+  }
+#pragma unroll
+  for (int i = 0; i < NPASS; ++i) {
     float acc = 0.0f;
 #pragma unroll
-    for (int t = 0; t < 8; ++t) acc = fmaf(static_cast<float>(a[t]), static_cast<float>(g[t]), acc);
+    for (int e = 0; e < 8; ++e) acc = fmaf(static_cast<float>(a[i][e]), static_cast<float>(g[i][e]), acc);
 #pragma unroll
     for (int off = LPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, LPR);
-    if (sub == 0) {
-      const int64_t t = row / H;
-      const int64_t h = row - t * H;
-      ndelta[h * T + t] = -acc;
-      lse2[h * T + t] = lse[h * T + t] * kLog2e;
-    }
+    if (sub == 0) sres[i * RPI + r] = acc;
+  }
+  __syncthreads();
+  const int64_t t = t0 + threadIdx.x;
+  if (threadIdx.x < kPreTokens && t < T) {
+    ndelta[h * T + t] = -sres[threadIdx.x];
+    lse2[h * T + t] = lse[h * T + t] * kLog2e;
   }
 }
 
@@ -44,19 +67,17 @@ __global__ __launch_bounds__(kThreads) void attn_bwd_pre_kernel(const bf16* __re
 
 hipError_t launch_bwd_pre(const AttnArgs& a, hipStream_t stream) {
   const int64_t rows = a.total_tokens * a.heads;
-  const int lpr = a.head_dim / 8;
-  const int64_t rpb = kThreads / lpr;
-  const int64_t want = (rows + rpb - 1) / rpb;
-  const dim3 grid(static_cast<unsigned>(want < 8192 ? want : 8192)), block(kThreads);
+  const int64_t ntb = (a.total_tokens + kPreTokens - 1) / kPreTokens;
+  const dim3 grid(static_cast<unsigned>(ntb * a.heads)), block(kThreads);
   const auto* o = static_cast<const bf16*>(a.out);
   const auto* g = static_cast<const bf16*>(a.dout);
   float* lse2 = a.delta + rows;
   if (a.head_dim == 128)
-    hipLaunchKernelGGL((attn_bwd_pre_kernel<128>), grid, block, 0, stream, o, g, a.lse, rows, a.heads,
-                       a.total_tokens, a.delta, lse2);
+    hipLaunchKernelGGL((attn_bwd_pre_kernel<128>), grid, block, 0, stream, o, g, a.lse, a.heads, a.total_tokens,
+                       a.delta, lse2);
   else
-    hipLaunchKernelGGL((attn_bwd_pre_kernel<64>), grid, block, 0, stream, o, g, a.lse, rows, a.heads,
-                       a.total_tokens, a.delta, lse2);
+    hipLaunchKernelGGL((attn_bwd_pre_kernel<64>), grid, block, 0, stream, o, g, a.lse, a.heads, a.total_tokens,
+                       a.delta, lse2);
   return hipGetLastError();
 }
 }  // namespace t2v
