@@ -379,8 +379,8 @@ def write_summaries(bench_json, sweep_jsonl=None):
               "bwd_dkdv q,k,v,dout,dk,dv + lse2, Delta; bwd_dq q,k,v,dout,dq + lse2, Delta.",
               "The MFMA kernels re-read K/V (fwd, dQ) or Q/dO (dK/dV) once per 128-row tile, mostly from L2 and",
               "the MALL; their HBM rates sit far below the 8 TB/s peak, so they are not bandwidth bound.",
-              "The Delta pass is HBM-bound; its 4-byte [H, T] stores are scattered, one (token, head) row per",
-              "16 lanes."]
+              "The Delta pass is HBM-bound; a workgroup owns one head and 64 consecutive tokens, so its [H, T]",
+              "stores and lse reads are contiguous 256-byte runs."]
     with open(os.path.join(ROOT, "profiles", "attn_fwd_bwd_hetero_hbm_counters.txt"), "w") as f:
         f.write("\n".join(lines) + "\n")
 
@@ -713,7 +713,8 @@ def run_workload(workload, seed, steps, warmup, order=None):
         if a and name in kf:
             entry["tflops"] = kf[name] / (a * 1e-3) * 1e-12
         if a and name == "bwd_pre":
-            entry["gbs"] = (4.0 * T * H * D + 4.0 * T * H) / (a * 1e-3) * 1e-9
+            # out and dout read (4 D bytes per (token, head)), lse read, -Delta and lse2 written
+            entry["gbs"] = (4.0 * T * H * D + 12.0 * T * H) / (a * 1e-3) * 1e-9
         kernels[name] = entry
     dominant = max((n for n in kf if avg.get(n)), key=lambda n: ktimes[n][0])
     achieved = kernels[dominant]["tflops"]
