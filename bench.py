@@ -497,6 +497,9 @@ def cost_model_sweep(steps: int = 4, warmup: int = 2):
 
     # One fit per model shape: the kernels' efficiency differs between head dims (the paper
     # likewise fits its regression coefficients for the model being trained).
+    lines.append("Command (repo root, on the GPU): python3 bench.py --cost-model")
+    lines.append(f"Kernel source hash (bench.py kernel_source_hash): {kernel_source_hash()}")
+    lines.append("")
     lines.append("Attention term of the DiT latency model (Section IV-B, Eq. (9)) on one MI355X (k = 1),")
     lines.append("fwd + bwd of libt2vattn in bf16, fitted per model shape of Table II:")
     lines.append("  t_ms = alpha2 * sum(L^2) + alpha1 * sum(L) + c0   (a bucket of B clips of S tokens: sum(L^2) = B*S^2)")
@@ -548,8 +551,8 @@ def plan_batch_report(n_gpus: int = 16, seed: int = 0):
 
     lengths = workload_shape("hetero", seed)[1]
     layers, H, D = 60, 24, 128
-    alpha2 = 4.734197e-08 * 1e-3 * layers        # s per token^2, attention fwd+bwd, all layers (fitted, 24 x 128)
-    alpha1_attn = 1.023822e-05 * 1e-3 * layers   # s per token (fitted)
+    alpha2 = 4.593638e-08 * 1e-3 * layers        # s per token^2, attention fwd+bwd, all layers (fitted, 24 x 128)
+    alpha1_attn = 8.631923e-06 * 1e-3 * layers   # s per token (fitted)
     alpha1_rest = 4 * 2 * 3 * (H * D) ** 2 * 12 / 1.0e15 * layers / (H * D)  # MLP+proj GEMMs at 1 PF/s, s/token
     hidden_bytes = H * D * 2
     a2a_bw = 7 * 153e9                           # xGMI: 7 links x ~153 GB/s per GPU
@@ -579,7 +582,8 @@ def plan_batch_report(n_gpus: int = 16, seed: int = 0):
     t0 = time.perf_counter()
     deg, starts, T = planner.plan(preds, K, lat, mem, W, n_gpus, population=64, generations=300, seed=seed)
     t_plan = time.perf_counter() - t0
-    lines = [f"Cascade plan of one batch: the heterogeneous mix (seed {seed}, {len(lengths)} clips) as {n} cascades "
+    lines = ["Command (repo root, CPU only): python3 bench.py --plan", "",
+             f"Cascade plan of one batch: the heterogeneous mix (seed {seed}, {len(lengths)} clips) as {n} cascades "
              f"on N = {n_gpus} GPUs, degrees K = {K} (Section IV-A, Eqs. (1)-(7); Alg. 1).",
              "Latency inputs: DiT attention from the MI355X cost model (24 x 128, 60 layers: alpha2 = "
              f"{alpha2:.3e} s/token^2, alpha1 = {alpha1_attn:.3e} s/token); assumed: rest of the block "
