@@ -26,12 +26,13 @@ if ROOT not in sys.path:
 METRIC = "varlen attention fwd+bwd TFLOP/s and % of bf16 MFMA peak, 1×MI355X"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
-# What decides the attention kernels' code and launches: device sources, the launch code, the
-# tile scheduler, and the HIP compile flags (the planner and other host-only code are left out).
+# What decides the attention kernels' code and launches: device sources with their launch
+# functions, the tile scheduler, and the HIP compile flags (argument validation, the work-list
+# cache, the planner and other host-only code are left out).
 KERNEL_SOURCES = ("paper_2607_01701_amd/csrc/t2v_fwd.hip", "paper_2607_01701_amd/csrc/t2v_bwd_pre.hip",
                   "paper_2607_01701_amd/csrc/t2v_bwd_dkdv.hip", "paper_2607_01701_amd/csrc/t2v_bwd_dq.hip",
                   "paper_2607_01701_amd/csrc/t2v_kernel_common.hpp", "paper_2607_01701_amd/csrc/t2v_device.hpp",
-                  "paper_2607_01701_amd/csrc/t2v_kernels.h", "paper_2607_01701_amd/csrc/t2v_api.hip",
+                  "paper_2607_01701_amd/csrc/t2v_kernels.h",
                   "paper_2607_01701_amd/csrc/t2v_host.cpp", "paper_2607_01701_amd/csrc/t2v_host.h")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 

@@ -27,7 +27,13 @@
  * Ownership. The caller owns every buffer. Tensor pointers are device
  * pointers; cu_seqlens is a HOST pointer (the tile scheduler runs on the
  * host). The library keeps only a cache of device work lists keyed by the
- * contents of cu_seqlens (released by t2v_release_cache).
+ * contents of cu_seqlens (released by t2v_release_cache). It holds up to 64;
+ * the call that adds one more releases the least recently used, which first
+ * waits for that list's device to finish its work.
+ *
+ * Threads. Calls from several host threads, on one stream or several, are
+ * safe: the cache is guarded by a mutex and a work list stays allocated while
+ * any call that looked it up is still enqueueing its launches.
  *
  * Errors. Every function returns a t2v_status. Arguments are validated before
  * anything is launched, so a rejected call writes nothing. Execution is

@@ -43,24 +43,29 @@ int check_host_pointer(const int32_t* cu) {
   return T2V_OK;
 }
 
-// Immutable device copies of work lists, keyed by everything that shapes them.
+// Immutable device copies of work lists, keyed by everything that shapes them. Calls hold
+// a shared reference from lookup until their launches are enqueued, so an entry evicted by
+// another thread meanwhile stays alive; the last reference frees it.
 struct Plan {
   std::vector<int32_t> cu, cu_loop;  // offsets of the owned and the looped-over segments
   int heads = 0, block = 0, order = 0, device = 0;
   Item* d_items = nullptr;
   Item* h_items = nullptr;  // pinned source of the upload, kept for the entry's life
   int n_items = 0;
-  hipEvent_t ready = nullptr;     // upload finished
-  hipEvent_t last_use = nullptr;  // last launch that read d_items
+  hipEvent_t ready = nullptr;  // upload finished
   ~Plan() {
-    if (last_use != nullptr) (void)hipEventSynchronize(last_use);
-    if (ready != nullptr) (void)hipEventSynchronize(ready);
+    // Launches on any stream may still read d_items: let the plan's device finish first.
+    int cur = -1;
+    const bool other = hipGetDevice(&cur) == hipSuccess && cur != device;
+    if (other) (void)hipSetDevice(device);
+    (void)hipDeviceSynchronize();
     if (d_items != nullptr) (void)hipFree(d_items);
     if (h_items != nullptr) (void)hipHostFree(h_items);
     if (ready != nullptr) (void)hipEventDestroy(ready);
-    if (last_use != nullptr) (void)hipEventDestroy(last_use);
+    if (other) (void)hipSetDevice(cur);
   }
 };
+using PlanRef = std::shared_ptr<Plan>;
 
 constexpr size_t kMaxPlans = 64;
 
@@ -69,10 +74,11 @@ class PlanCache {
   // Returns the plan (creating and uploading it on `stream` if new) with the
   // upload ordered before any later work on `stream`.
   int get(const int32_t* cu, const int32_t* cu_loop, int nseq, int heads, int block, int order, hipStream_t stream,
-          Plan** out) {
+          PlanRef* out) {
     int device = 0;
     hipError_t e = hipGetDevice(&device);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    std::list<PlanRef> evicted;  // declared before the lock: released after it
     std::lock_guard<std::mutex> lock(mu_);
     for (auto itr = plans_.begin(); itr != plans_.end(); ++itr) {
       Plan& p = **itr;
@@ -83,11 +89,11 @@ class PlanCache {
         plans_.splice(plans_.begin(), plans_, itr);  // most recently used first
         e = hipStreamWaitEvent(stream, p.ready, 0);
         if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
-        *out = &p;
+        *out = *itr;
         return T2V_OK;
       }
     }
-    std::unique_ptr<Plan> p(new Plan());
+    PlanRef p = std::make_shared<Plan>();
     p->cu.assign(cu, cu + nseq + 1);
     p->cu_loop.assign(cu_loop, cu_loop + nseq + 1);
     p->heads = heads;
@@ -112,35 +118,34 @@ class PlanCache {
     }
     e = hipEventCreateWithFlags(&p->ready, hipEventDisableTiming);
     if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
-    e = hipEventCreateWithFlags(&p->last_use, hipEventDisableTiming);
-    if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
     if (bytes > 0) {
       e = hipMemcpyAsync(p->d_items, p->h_items, bytes, hipMemcpyHostToDevice, stream);
       if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync of the work list");
     }
     e = hipEventRecord(p->ready, stream);
     if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
-    plans_.push_front(std::move(p));
-    while (plans_.size() > kMaxPlans) plans_.pop_back();  // waits for the evicted plan's last use
-    *out = plans_.front().get();
-    return T2V_OK;
-  }
-
-  int mark_used(Plan* p, hipStream_t stream) {
-    std::lock_guard<std::mutex> lock(mu_);
-    const hipError_t e = hipEventRecord(p->last_use, stream);
-    if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+    plans_.push_front(p);
+    *out = p;
+    // An evicted plan is freed (after its device finishes) when its last reference goes:
+    // here after the lock is released, or later by a call still holding it.
+    while (plans_.size() > kMaxPlans) {
+      evicted.push_back(std::move(plans_.back()));
+      plans_.pop_back();
+    }
     return T2V_OK;
   }
 
   void clear() {
-    std::lock_guard<std::mutex> lock(mu_);
-    plans_.clear();
+    std::list<PlanRef> old;
+    {
+      std::lock_guard<std::mutex> lock(mu_);
+      old.swap(plans_);
+    }
   }
 
  private:
   std::mutex mu_;
-  std::list<std::unique_ptr<Plan>> plans_;
+  std::list<PlanRef> plans_;
 };
 
 PlanCache& cache() {
@@ -248,7 +253,7 @@ int attn_fwd_impl(const void* q, const void* k, const void* v, const int32_t* cu
   if (cu_k != cu_q)
     if (int st = check_host_pointer(cu_k)) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  Plan* plan = nullptr;
+  PlanRef plan;
   if (int st = cache().get(cu_q, cu_k, nseq, heads, fwd_tile_rows(head_dim), order_from_env(), s, &plan)) return st;
   if (plan->n_items == 0) return T2V_OK;
   AttnArgs a{};
@@ -261,7 +266,7 @@ int attn_fwd_impl(const void* q, const void* k, const void* v, const int32_t* cu
   a.scale = scale;
   hipError_t e = timer().run(kSlotFwd, s, [&] { return launch_fwd(a, out, lse, plan->d_items, plan->n_items, s); });
   if (e != hipSuccess) return hip_fail(e, "forward kernel launch");
-  return cache().mark_used(plan, s);
+  return T2V_OK;
 }
 
 int attn_bwd_impl(const void* q, const void* k, const void* v, const void* out, const float* lse, const int32_t* cu_q,
@@ -286,8 +291,7 @@ int attn_bwd_impl(const void* q, const void* k, const void* v, const void* out, 
     if (int st = check_host_pointer(cu_k)) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int order = order_from_env();
-  Plan* pk = nullptr;
-  Plan* pq = nullptr;
+  PlanRef pk, pq;
   // dK/dV tiles own keys and loop over queries; dQ tiles own queries and loop over keys.
   if (int st = cache().get(cu_k, cu_q, nseq, heads, dkdv_tile_rows(head_dim), order, s, &pk)) return st;
   if (int st = cache().get(cu_q, cu_k, nseq, heads, dq_tile_rows(head_dim), order, s, &pq)) return st;
@@ -316,8 +320,7 @@ int attn_bwd_impl(const void* q, const void* k, const void* v, const void* out, 
     e = timer().run(kSlotDq, s, [&] { return launch_bwd_dq(a, pq->d_items, pq->n_items, s); });
     if (e != hipSuccess) return hip_fail(e, "dQ kernel launch");
   }
-  if (int st = cache().mark_used(pk, s)) return st;
-  return cache().mark_used(pq, s);
+  return T2V_OK;
 }
 
 // Runs f, turning host exceptions into statuses (none may cross the C ABI).
