@@ -78,6 +78,9 @@ def parse_args():
                     help="(CPU) plan one training batch of the heterogeneous mix as a cascade DAG on N GPUs with the "
                          "native genetic-algorithm planner; attention latency from the fitted cost model; compares "
                          "against static parallel degrees and prints a text report")
+    ap.add_argument("--balance", action="store_true",
+                    help="trace one fwd+bwd step per scheduler order and print each kernel's per-CU busy-time "
+                         "CV and idle share (the library's workgroup trace)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain device copy of known size (for HBM counter scaling)")
     ap.add_argument("--ingest-rocpd", nargs=5, metavar=("KT_DB", "FETCH_DB", "WRITE_DB", "COPY_FETCH_DB",
@@ -533,6 +536,77 @@ def cost_model_sweep(steps: int = 4, warmup: int = 2):
     return "\n".join(lines)
 
 
+def balance_report(workload: str = "hetero", seed: int = 0):
+    """Per-CU balance of each attention kernel on one traced fwd+bwd step, for both scheduler
+    orders: per-CU busy time (summed workgroup durations from the library's workgroup trace),
+    its coefficient of variation over the CUs (the single-GPU analogue of the per-rank CV of
+    the paper's case study, Section V-E), and the idle share of CU time within the kernel's
+    span; beside it the host scheduler's own predicted makespan over its lower bound."""
+    import numpy as np
+    import torch
+
+    from paper_2607_01701_amd import _lib
+    from paper_2607_01701_amd.workload import DESCRIPTIONS, make_workload
+
+    pack = make_workload(workload, seed=seed)
+    H, D, T = pack.heads, pack.head_dim, pack.total_tokens
+
+    def dev(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
+
+    q, k, v, g = dev(pack.q), dev(pack.k), dev(pack.v), dev(pack.dout)
+    ncu = torch.cuda.get_device_properties(0).multi_processor_count
+    lines = ["Command (repo root, on the GPU): python3 bench.py --balance",
+             f"Kernel source hash (bench.py kernel_source_hash): {kernel_source_hash()}", "",
+             f"Per-CU balance of one traced fwd+bwd step, {workload} workload ({DESCRIPTIONS[workload]}), "
+             f"{ncu} CUs.",
+             "busy = summed durations of the workgroups a CU ran; CV = std / mean of busy over the CUs; "
+             "idle = 1 - sum(busy) / (CUs x kernel span);",
+             "host LPT = the scheduler's predicted list-scheduling makespan over its lower bound "
+             "(max(total / slots, largest item)) for the same work list.", "",
+             f"{'order':14s} {'kernel':9s} {'WGs':>6s} {'CUs':>4s} {'span ms':>8s} {'busy mean ms':>12s} "
+             f"{'CV':>6s} {'idle':>6s} {'host LPT':>9s}"]
+    rows = {"fwd": 256, "bwd_dkdv": 128, "bwd_dq": 256}
+    names = {0: "fwd", 2: "bwd_dkdv", 3: "bwd_dq"}
+    for order in ("longest_first", "natural"):
+        os.environ["T2V_ORDER"] = order
+        _lib.attn_fwd(q, k, v, pack.cu_seqlens, pack.scale)  # builds and caches the work lists
+        cap = sum(_lib.t2v_build_worklist(pack.cu_seqlens, H, r,
+                                          _lib.ORDER_NATURAL if order == "natural" else _lib.ORDER_LONGEST_FIRST
+                                          ).shape[0] for r in rows.values())
+        rec = torch.zeros(4 * cap, dtype=torch.int64, device="cuda")
+        torch.cuda.synchronize()
+        _lib.t2v_trace_set(rec.data_ptr(), cap)
+        try:
+            out, lse = _lib.attn_fwd(q, k, v, pack.cu_seqlens, pack.scale)
+            _lib.attn_bwd(q, k, v, out, lse, g, pack.cu_seqlens, pack.scale)
+            torch.cuda.synchronize()
+            n, over = _lib.t2v_trace_count()
+        finally:
+            _lib.t2v_trace_set(None, 0)
+        if n != cap or over:
+            raise SystemExit(f"trace took {n} of {cap} records ({over} launches did not fit)")
+        r = rec.view(cap, 4).cpu().numpy().astype(np.int64)
+        for slot, name in names.items():
+            x = r[r[:, 3] == slot]
+            t0, t1 = x[:, 1], x[:, 2]
+            span = float(t1.max() - t0.min())
+            busy = {}
+            for cu, d in zip(x[:, 0], t1 - t0):
+                busy[cu] = busy.get(cu, 0) + int(d)
+            b = np.array(list(busy.values()), dtype=np.float64)
+            b = np.concatenate([b, np.zeros(max(0, ncu - len(b)))])  # CUs that ran nothing
+            items = _lib.t2v_build_worklist(pack.cu_seqlens, H, rows[name],
+                                            _lib.ORDER_NATURAL if order == "natural" else _lib.ORDER_LONGEST_FIRST)
+            mk, lb = _lib.t2v_plan_makespan(items, rows[name], ncu)
+            lines.append(f"{order:14s} {name:9s} {x.shape[0]:6d} {len(busy):4d} {span * 1e-5:8.3f} "
+                         f"{b.mean() * 1e-5:12.3f} {b.std() / b.mean():6.3f} {1 - b.sum() / (ncu * span):6.1%} "
+                         f"{mk / lb:9.3f}")
+    os.environ.pop("T2V_ORDER", None)
+    lines += ["", "(device clock 100 MHz: 1 tick = 10 ns)"]
+    return "\n".join(lines)
+
+
 def plan_batch_report(n_gpus: int = 16, seed: int = 0):
     """Cascade plan of one batch (paper Section IV-A, Eqs. (1)-(7); Alg. 1) on the CPU.
 
@@ -816,6 +890,9 @@ def main():
 
     if args.cost_model:
         print(cost_model_sweep(), flush=True)
+        return
+    if args.balance:
+        print(balance_report(args.workload, args.seed), flush=True)
         return
     if args.sweep:
         # Smaller step counts for the long workloads keep the sweep to about a minute of GPU time.

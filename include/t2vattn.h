@@ -185,6 +185,22 @@ int t2v_plan_cascades(int n_cascades, const int32_t* pred_ptr, const int32_t* pr
 int t2v_timing_enable(int on);
 int t2v_kernel_times(double* ms_out, int* counts_out);
 
+/* Per-workgroup trace, for measurement: the single-GPU analogue of the per-rank balance
+ * metric of the case study (Section V-E), i.e. per-CU busy time and its coefficient of
+ * variation. While armed, every forward, dK/dV and dQ kernel launch takes the next n_items
+ * records of dev_records, one per workgroup in work-list order, each four uint64:
+ * {CU id, start, end, kernel slot}; CU id = (XCC_ID << 16) | bits 8..15 of HW_ID, start
+ * and end on the constant 100 MHz device clock, slot 0 forward, 2 dK/dV, 3 dQ. A launch
+ * whose records do not fit runs untraced and is counted as overflowed. Tracing does not
+ * change any result.
+ *   dev_records  device unsigned long long[4 * capacity], 8-byte aligned, caller-owned;
+ *                NULL (with capacity 0) disarms
+ *   t2v_trace_set resets the count; t2v_trace_count returns the records taken so far and
+ *   the number of launches that did not fit.
+ * Invalid arguments: T2V_ERR_INVALID_ARG. */
+int t2v_trace_set(unsigned long long* dev_records, int64_t capacity);
+int t2v_trace_count(int64_t* n_records, int* n_overflowed);
+
 /* MFMA throughput probe, for measurement context only (not part of the attention path).
  * Launches `blocks` workgroups of four waves; each wave runs four independent chains of
  * `iters` v_mfma_f32_32x32x16_bf16 with no memory traffic, on `stream`, and waits for it.

@@ -29,7 +29,8 @@ ORDER_LONGEST_FIRST = 1
 # Symbols declared in include/t2vattn.h.
 EXPORTS = ("t2v_attn_fwd", "t2v_attn_bwd", "t2v_attn_fwd_qk", "t2v_attn_bwd_qk", "t2v_last_error",
            "t2v_release_cache", "t2v_build_worklist", "t2v_plan_makespan", "t2v_timing_enable", "t2v_kernel_times",
-           "t2v_version", "t2v_list_schedule", "t2v_plan_cascades", "t2v_probe_mfma_peak")
+           "t2v_version", "t2v_list_schedule", "t2v_plan_cascades", "t2v_probe_mfma_peak", "t2v_trace_set",
+           "t2v_trace_count")
 KERNEL_SLOTS = ("fwd", "bwd_pre", "bwd_dkdv", "bwd_dq")
 HOST_EXPORTS = ("t2v_last_error", "t2v_build_worklist", "t2v_plan_makespan", "t2v_version", "t2v_list_schedule",
                 "t2v_plan_cascades")
@@ -83,6 +84,10 @@ def _declare(lib, full: bool):
         lib.t2v_kernel_times.restype = ctypes.c_int
         lib.t2v_kernel_times.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int)]
         lib.t2v_probe_mfma_peak.restype = ctypes.c_int
+        lib.t2v_trace_set.restype = ctypes.c_int
+        lib.t2v_trace_set.argtypes = [_vp, ctypes.c_int64]
+        lib.t2v_trace_count.restype = ctypes.c_int
+        lib.t2v_trace_count.argtypes = [ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_int)]
         lib.t2v_probe_mfma_peak.argtypes = [_vp, ctypes.c_int, ctypes.c_int, _vp, _dp, _dp, _dp]
     return lib
 
@@ -180,6 +185,18 @@ def t2v_probe_mfma_peak(rec, blocks: int, iters: int, stream) -> dict:
     _check(lib(), lib().t2v_probe_mfma_peak(rec, int(blocks), int(iters), stream, ctypes.byref(ms),
                                             ctypes.byref(tf), ctypes.byref(ghz)))
     return {"ms": ms.value, "tflops": tf.value, "ghz": ghz.value}
+
+
+def t2v_trace_set(dev_records, capacity: int) -> None:
+    """Arms (device address of 4 * capacity uint64) or disarms (None, 0) the workgroup trace."""
+    _check(lib(), lib().t2v_trace_set(dev_records, int(capacity)))
+
+
+def t2v_trace_count() -> tuple:
+    """(records taken since the trace was armed, launches that did not fit)."""
+    n, o = ctypes.c_int64(), ctypes.c_int()
+    _check(lib(), lib().t2v_trace_count(ctypes.byref(n), ctypes.byref(o)))
+    return n.value, o.value
 
 
 def t2v_version(L=None) -> str:

@@ -228,6 +228,47 @@ KernelTimer& timer() {
   return *t;
 }
 
+// Optional per-workgroup trace: while armed, each MFMA kernel launch takes the next
+// n_items records of the caller's buffer (4 uint64 each); a launch that does not fit is
+// run untraced and counted as overflowed.
+class WorkgroupTracer {
+ public:
+  void set(unsigned long long* buf, int64_t capacity) {
+    std::lock_guard<std::mutex> lock(mu_);
+    buf_ = buf;
+    cap_ = buf != nullptr ? capacity : 0;
+    used_ = 0;
+    overflow_ = 0;
+  }
+  unsigned long long* reserve(int64_t n) {
+    std::lock_guard<std::mutex> lock(mu_);
+    if (buf_ == nullptr || n <= 0) return nullptr;
+    if (used_ + n > cap_) {
+      ++overflow_;
+      return nullptr;
+    }
+    unsigned long long* p = buf_ + 4 * used_;
+    used_ += n;
+    return p;
+  }
+  void count(int64_t* used, int* overflow) {
+    std::lock_guard<std::mutex> lock(mu_);
+    *used = used_;
+    *overflow = overflow_;
+  }
+
+ private:
+  std::mutex mu_;
+  unsigned long long* buf_ = nullptr;
+  int64_t cap_ = 0, used_ = 0;
+  int overflow_ = 0;
+};
+
+WorkgroupTracer& tracer() {
+  static WorkgroupTracer* t = new WorkgroupTracer();
+  return *t;
+}
+
 }  // namespace
 }  // namespace t2v
 
@@ -264,6 +305,7 @@ int attn_fwd_impl(const void* q, const void* k, const void* v, const int32_t* cu
   a.head_dim = head_dim;
   a.total_tokens = Tq;
   a.scale = scale;
+  a.trace = tracer().reserve(plan->n_items);
   hipError_t e = timer().run(kSlotFwd, s, [&] { return launch_fwd(a, out, lse, plan->d_items, plan->n_items, s); });
   if (e != hipSuccess) return hip_fail(e, "forward kernel launch");
   return T2V_OK;
@@ -313,10 +355,12 @@ int attn_bwd_impl(const void* q, const void* k, const void* v, const void* out, 
   hipError_t e = timer().run(kSlotPre, s, [&] { return launch_bwd_pre(a, s); });
   if (e != hipSuccess) return hip_fail(e, "backward preprocess launch");
   if (pk->n_items > 0) {
+    a.trace = tracer().reserve(pk->n_items);
     e = timer().run(kSlotDkdv, s, [&] { return launch_bwd_dkdv(a, pk->d_items, pk->n_items, s); });
     if (e != hipSuccess) return hip_fail(e, "dK/dV kernel launch");
   }
   if (pq->n_items > 0) {
+    a.trace = tracer().reserve(pq->n_items);
     e = timer().run(kSlotDq, s, [&] { return launch_bwd_dq(a, pq->d_items, pq->n_items, s); });
     if (e != hipSuccess) return hip_fail(e, "dQ kernel launch");
   }
@@ -385,6 +429,21 @@ int t2v_timing_enable(int on) {
 int t2v_kernel_times(double* ms_out, int* counts_out) {
   if (ms_out == nullptr || counts_out == nullptr) return t2v::set_error(T2V_ERR_INVALID_ARG, "NULL output");
   return t2v::timer().read(ms_out, counts_out);
+}
+
+int t2v_trace_set(unsigned long long* dev_records, int64_t capacity) {
+  if (capacity < 0 || (dev_records == nullptr && capacity != 0))
+    return t2v::set_error(T2V_ERR_INVALID_ARG, "capacity must be >= 0, and 0 when dev_records is NULL");
+  if (dev_records != nullptr && reinterpret_cast<uintptr_t>(dev_records) % 8 != 0)
+    return t2v::set_error(T2V_ERR_INVALID_ARG, "dev_records is not 8-byte aligned");
+  t2v::tracer().set(dev_records, capacity);
+  return T2V_OK;
+}
+
+int t2v_trace_count(int64_t* n_records, int* n_overflowed) {
+  if (n_records == nullptr || n_overflowed == nullptr) return t2v::set_error(T2V_ERR_INVALID_ARG, "NULL output");
+  t2v::tracer().count(n_records, n_overflowed);
+  return T2V_OK;
 }
 
 void t2v_release_cache(void) {

@@ -127,7 +127,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
     const bf16* __restrict__ dout, const float* __restrict__ lse2, const float* __restrict__ ndelta,
     const Item* __restrict__ items, int H, int64_t T, float c, float scale, bf16* __restrict__ dk,
-    bf16* __restrict__ dv) {
+    bf16* __restrict__ dv, unsigned long long* __restrict__ trace) {
+  const unsigned long long trace_t0 = trace != nullptr ? trace_clock() : 0ull;
   constexpr int KK = D / 16;
   constexpr int DB = D / 32;
   constexpr int BM = kDkdvBM;      // queries per LDS stage
@@ -260,6 +261,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
       }
     }
   }
+  if (trace != nullptr) trace_end(trace, trace_t0, 2);
 }
 
 }  // namespace
@@ -278,10 +280,10 @@ hipError_t launch_bwd_dkdv(const AttnArgs& a, const Item* items, int n_items, hi
   const float* lse2 = a.delta + a.total_tokens * a.heads;
   if (a.head_dim == 128)
     hipLaunchKernelGGL((attn_bwd_dkdv_kernel<128>), grid, block, 0, stream, q, k, v, g, lse2, a.delta, items,
-                       a.heads, a.total_tokens, c, a.scale, dk, dv);
+                       a.heads, a.total_tokens, c, a.scale, dk, dv, a.trace);
   else
     hipLaunchKernelGGL((attn_bwd_dkdv_kernel<64>), grid, block, 0, stream, q, k, v, g, lse2, a.delta, items,
-                       a.heads, a.total_tokens, c, a.scale, dk, dv);
+                       a.heads, a.total_tokens, c, a.scale, dk, dv, a.trace);
   return hipGetLastError();
 }
 }  // namespace t2v

@@ -84,7 +84,9 @@ template <int D, int QB>
 __global__ __launch_bounds__(kDqThreads, 1) void attn_bwd_dq_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
     const bf16* __restrict__ dout, const float* __restrict__ lse2, const float* __restrict__ ndelta,
-    const Item* __restrict__ items, int H, int64_t T, float c, float scale, bf16* __restrict__ dq) {
+    const Item* __restrict__ items, int H, int64_t T, float c, float scale, bf16* __restrict__ dq,
+    unsigned long long* __restrict__ trace) {
+  const unsigned long long trace_t0 = trace != nullptr ? trace_clock() : 0ull;
   constexpr int KK = D / 16;
   constexpr int DB = D / 32;
   constexpr int BN = kDqBN;  // keys per LDS stage
@@ -187,6 +189,7 @@ __global__ __launch_bounds__(kDqThreads, 1) void attn_bwd_dq_kernel(
       }
     }
   }
+  if (trace != nullptr) trace_end(trace, trace_t0, 3);
 }
 
 }  // namespace
@@ -204,10 +207,10 @@ hipError_t launch_bwd_dq(const AttnArgs& a, const Item* items, int n_items, hipS
   const float* lse2 = a.delta + a.total_tokens * a.heads;
   if (a.head_dim == 128)
     hipLaunchKernelGGL((attn_bwd_dq_kernel<128, kDqQB>), grid, block, 0, stream, q, k, v, g, lse2, a.delta,
-                       items, a.heads, a.total_tokens, c, a.scale, dq);
+                       items, a.heads, a.total_tokens, c, a.scale, dq, a.trace);
   else
     hipLaunchKernelGGL((attn_bwd_dq_kernel<64, kDqQB>), grid, block, 0, stream, q, k, v, g, lse2, a.delta,
-                       items, a.heads, a.total_tokens, c, a.scale, dq);
+                       items, a.heads, a.total_tokens, c, a.scale, dq, a.trace);
   return hipGetLastError();
 }
 }  // namespace t2v

@@ -277,6 +277,30 @@ T2V_DEV bf16x8 read_rows_opnd(uint32_t base0, uint32_t base1, int row0, int db) 
   return out;
 }
 
+// ---------------------------------------------------------------- workgroup trace
+//
+// Measurement only. When a launch is traced, each workgroup writes one record of four
+// uint64 at rec + 4 * blockIdx.x: the CU it ran on ((XCC_ID << 16) | HW_ID bits 8..15,
+// i.e. CU, shader array and shader engine within the XCD), its start and end on the
+// constant 100 MHz clock, and the kernel's slot.
+T2V_DEV unsigned long long trace_clock() { return __builtin_amdgcn_s_memrealtime(); }
+
+// Every wave of the workgroup must call this (it holds a barrier); rec is uniform.
+T2V_DEV void trace_end(unsigned long long* rec, unsigned long long t0, int slot) {
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    unsigned hw, xcc;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_HW_ID)" : "=s"(hw));
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+    const unsigned long long t1 = __builtin_amdgcn_s_memrealtime();
+    unsigned long long* r = rec + 4 * static_cast<size_t>(blockIdx.x);
+    r[0] = (static_cast<unsigned long long>(xcc & 0xFu) << 16) | ((hw >> 8) & 0xFFu);
+    r[1] = t0;
+    r[2] = t1;
+    r[3] = static_cast<unsigned long long>(slot);
+  }
+}
+
 // Eight fp32 to packed bf16 (round to nearest even, v_cvt_pk_bf16_f32).
 T2V_DEV bf16x8 to_bf16x8(const f32x16& x, int base) {
   bf16x8 r;

@@ -143,7 +143,8 @@ template <int D, int QB, bool NEG>
 __global__ __launch_bounds__(kFwdThreads, 1) void attn_fwd_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
     const Item* __restrict__ items, int H, int64_t T, float c, bf16* __restrict__ out,
-    float* __restrict__ lse) {
+    float* __restrict__ lse, unsigned long long* __restrict__ trace) {
+  const unsigned long long trace_t0 = trace != nullptr ? trace_clock() : 0ull;
   constexpr int KK = D / 16;  // k-steps of the head-dim contraction
   constexpr int DB = D / 32;  // 32-wide head-dim blocks of the output
   constexpr int BN = kFwdBN;  // keys per LDS stage
@@ -247,6 +248,7 @@ __global__ __launch_bounds__(kFwdThreads, 1) void attn_fwd_kernel(
       }
     }
   }
+  if (trace != nullptr) trace_end(trace, trace_t0, 0);
 }
 
 }  // namespace
@@ -265,17 +267,17 @@ hipError_t launch_fwd(const AttnArgs& a, void* out, float* lse, const Item* item
   if (a.head_dim == 128) {
     if (neg)
       hipLaunchKernelGGL((attn_fwd_kernel<128, kFwdQB, true>), grid, block, 0, stream, q, k, v, items, a.heads,
-                         a.total_tokens, c, o, lse);
+                         a.total_tokens, c, o, lse, a.trace);
     else
       hipLaunchKernelGGL((attn_fwd_kernel<128, kFwdQB, false>), grid, block, 0, stream, q, k, v, items, a.heads,
-                         a.total_tokens, c, o, lse);
+                         a.total_tokens, c, o, lse, a.trace);
   } else {
     if (neg)
       hipLaunchKernelGGL((attn_fwd_kernel<64, kFwdQB, true>), grid, block, 0, stream, q, k, v, items, a.heads,
-                         a.total_tokens, c, o, lse);
+                         a.total_tokens, c, o, lse, a.trace);
     else
       hipLaunchKernelGGL((attn_fwd_kernel<64, kFwdQB, false>), grid, block, 0, stream, q, k, v, items, a.heads,
-                         a.total_tokens, c, o, lse);
+                         a.total_tokens, c, o, lse, a.trace);
   }
   return hipGetLastError();
 }

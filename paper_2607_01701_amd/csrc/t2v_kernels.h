@@ -29,6 +29,8 @@ struct AttnArgs {
   int head_dim;
   int64_t total_tokens;
   float scale;
+  // Per-workgroup trace records of the launch being made (4 uint64 each), or nullptr.
+  unsigned long long* trace = nullptr;
 };
 
 hipError_t launch_fwd(const AttnArgs& a, void* out, float* lse, const Item* items, int n_items,

@@ -209,3 +209,15 @@ def test_mfma_probe_validation():
         assert L.t2v_probe_mfma_peak(fake, blocks, iters, None, ref, ref, ref) == _lib.T2V_ERR_INVALID_ARG
         assert "blocks must be" in _lib.t2v_last_error(L)
     assert L.t2v_probe_mfma_peak(fake, 4, 10, None, None, ref, ref) == _lib.T2V_ERR_INVALID_ARG
+
+
+def test_trace_set_validation():
+    """The workgroup trace rejects a negative capacity, a capacity without a buffer and a
+    misaligned buffer; disarming (NULL, 0) is always accepted."""
+    L = _lib.lib()
+    assert L.t2v_trace_set(None, -1) == _lib.T2V_ERR_INVALID_ARG
+    assert L.t2v_trace_set(None, 5) == _lib.T2V_ERR_INVALID_ARG
+    assert L.t2v_trace_set(ctypes.c_void_p(4100), 5) == _lib.T2V_ERR_INVALID_ARG  # not 8-byte aligned
+    assert "aligned" in _lib.t2v_last_error(L)
+    assert L.t2v_trace_set(None, 0) == _lib.T2V_OK
+    assert _lib.t2v_trace_count() == (0, 0)
