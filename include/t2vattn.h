@@ -31,6 +31,11 @@
  * the call that adds one more releases the least recently used, which first
  * waits for that list's device to finish its work.
  *
+ * Environment. T2V_ORDER=natural schedules tiles in pack order instead of longest clip
+ * first (for ablations). T2V_LOG=1 prints one line to stderr per new work list: its items,
+ * the host's predicted list-scheduling makespan and its lower bound. T2V_TEST_FAIL_ALLOC=1
+ * makes building a new work list fail with T2V_ERR_OOM, for testing that path.
+ *
  * Threads. Calls from several host threads, on one stream or several, are
  * safe: the cache is guarded by a mutex and a work list stays allocated while
  * any call that looked it up is still enqueueing its launches.

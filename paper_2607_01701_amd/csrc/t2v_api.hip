@@ -2,6 +2,7 @@
 #include <hip/hip_runtime.h>
 
 #include <atomic>
+#include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <list>
@@ -27,6 +28,19 @@ int order_from_env() {
   const char* s = std::getenv("T2V_ORDER");
   if (s != nullptr && std::strcmp(s, "natural") == 0) return T2V_ORDER_NATURAL;
   return T2V_ORDER_LONGEST_FIRST;
+}
+
+// T2V_LOG=1: one line on stderr per new work list (items, predicted makespan, bound).
+bool log_enabled() {
+  const char* s = std::getenv("T2V_LOG");
+  return s != nullptr && std::strcmp(s, "1") == 0;
+}
+
+// T2V_TEST_FAIL_ALLOC=1 makes the work-list allocation fail, so callers can exercise the
+// T2V_ERR_OOM path (nothing is launched and the cache is unchanged).
+bool fail_alloc_for_test() {
+  const char* s = std::getenv("T2V_TEST_FAIL_ALLOC");
+  return s != nullptr && std::strcmp(s, "1") == 0;
 }
 
 // cu_seqlens must be host memory: the scheduler reads it on the host.
@@ -103,6 +117,18 @@ class PlanCache {
     std::vector<Item> items = build_worklist(cu, cu_loop, nseq, heads, block, order);
     p->n_items = static_cast<int>(items.size());
     const size_t bytes = items.size() * sizeof(Item);
+    if (log_enabled()) {
+      int ncu = 0;
+      (void)hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, device);
+      double ms = 0.0, lb = 0.0;
+      plan_makespan(items.data(), p->n_items, block, ncu > 0 ? ncu : 1, &ms, &lb);
+      std::fprintf(stderr,
+                   "t2v: work list: %d sequences, %d heads, %d-row tiles, %s order: %d items, predicted makespan "
+                   "%.4g (lower bound %.4g, ratio %.4f) on %d CUs\n",
+                   nseq, heads, block, order == T2V_ORDER_NATURAL ? "pack" : "longest-first", p->n_items, ms, lb,
+                   lb > 0.0 ? ms / lb : 1.0, ncu);
+    }
+    if (bytes > 0 && fail_alloc_for_test()) return set_error(T2V_ERR_OOM, "hipMalloc of the work list failed (forced)");
     if (bytes > 0) {
       e = hipMalloc(&p->d_items, bytes);
       if (e != hipSuccess) {

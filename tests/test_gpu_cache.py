@@ -79,3 +79,35 @@ def test_threads_on_their_own_streams():
     torch.cuda.synchronize()
     for i in range(4):
         assert same(alone[i], results[i]), f"thread {i} differs from the single-threaded result"
+
+
+def test_log_prints_the_plan_summary(monkeypatch, capfd):
+    import torch
+    from paper_2607_01701_amd import attn_fwd
+    monkeypatch.setenv("T2V_LOG", "1")
+    pack = make_pack([777, 41], 2, 64, seed=90)  # lengths no other test uses: a new work list
+    d = dev_inputs(pack)
+    attn_fwd(d["q"], d["k"], d["v"], pack.cu_seqlens, pack.scale)
+    torch.cuda.synchronize()
+    err = capfd.readouterr().err
+    assert "t2v: work list: 2 sequences, 2 heads, 256-row tiles, longest-first order: 10 items" in err, err
+    assert "predicted makespan" in err and "lower bound" in err
+
+
+def test_forced_allocation_failure_is_reported_and_recovers(monkeypatch):
+    import torch
+    from paper_2607_01701_amd import _lib, attn_fwd
+    pack = make_pack([611, 29], 2, 128, seed=91)  # a new work list
+    d = dev_inputs(pack)
+    out = torch.full_like(d["q"], 7.0)
+    monkeypatch.setenv("T2V_TEST_FAIL_ALLOC", "1")
+    with pytest.raises(_lib.T2VError) as ei:
+        attn_fwd(d["q"], d["k"], d["v"], pack.cu_seqlens, pack.scale, out=out)
+    assert ei.value.status == _lib.T2V_ERR_OOM and "forced" in str(ei.value)
+    torch.cuda.synchronize()
+    assert bool((out == 7.0).all()), "a failed call wrote its output"
+    monkeypatch.delenv("T2V_TEST_FAIL_ALLOC")
+    o1, _ = attn_fwd(d["q"], d["k"], d["v"], pack.cu_seqlens, pack.scale)
+    o2, _ = attn_fwd(d["q"], d["k"], d["v"], pack.cu_seqlens, pack.scale)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2)
