@@ -1,0 +1,173 @@
+// Randomised exercise of the host-side code of libt2vattn (tile scheduler, makespan model,
+// argument validation, cascade planner), built with AddressSanitizer and
+// UndefinedBehaviorSanitizer by tests/test_host_sanitizers.py. Every check that fails prints
+// a line; the exit status is the number of failed checks (sanitizer reports abort earlier).
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstdio>
+#include <random>
+#include <string>
+#include <vector>
+
+#include "../include/t2vattn.h"
+#include "../paper_2607_01701_amd/csrc/t2v_host.h"
+
+static int g_failed = 0;
+#define CHECK(cond, what)                                              \
+  do {                                                                 \
+    if (!(cond)) {                                                     \
+      ++g_failed;                                                      \
+      std::printf("FAIL %s:%d %s\n", __FILE__, __LINE__, (what));      \
+    }                                                                  \
+  } while (0)
+
+static std::vector<int32_t> random_cu(std::mt19937& rng, int nseq, int max_len) {
+  std::vector<int32_t> cu(nseq + 1, 0);
+  std::uniform_int_distribution<int> len(0, max_len), zero(0, 4);
+  for (int s = 0; s < nseq; ++s) cu[s + 1] = cu[s] + (zero(rng) == 0 ? 0 : len(rng));
+  return cu;
+}
+
+// Work lists: every (clip, head, tile) exactly once, tiles cover the clip, a short buffer
+// is refused, and the makespan model respects its own lower bound.
+static void worklists(std::mt19937& rng) {
+  for (int rep = 0; rep < 300; ++rep) {
+    const int nseq = std::uniform_int_distribution<int>(0, 40)(rng);
+    const int heads = std::uniform_int_distribution<int>(1, 8)(rng);
+    const int block = rep % 2 ? 128 : 256;
+    const int order = rep % 3 == 0 ? T2V_ORDER_NATURAL : T2V_ORDER_LONGEST_FIRST;
+    const std::vector<int32_t> cu = random_cu(rng, nseq, 5000);
+    int n = -1;
+    CHECK(t2v_build_worklist(cu.data(), nseq, heads, block, order, nullptr, 0, &n) == T2V_OK, "count query");
+    int64_t expect = 0;
+    for (int s = 0; s < nseq; ++s) expect += int64_t(heads) * ((cu[s + 1] - cu[s] + block - 1) / block);
+    CHECK(n == expect, "item count");
+    std::vector<int32_t> items(4 * static_cast<size_t>(n) + 4, -7);
+    if (n > 0) {
+      int m = 0;
+      CHECK(t2v_build_worklist(cu.data(), nseq, heads, block, order, items.data(), n - 1, &m) ==
+                T2V_ERR_INVALID_ARG, "short buffer refused");
+    }
+    CHECK(t2v_build_worklist(cu.data(), nseq, heads, block, order, items.data(), n, &n) == T2V_OK, "fill");
+    CHECK(items[4 * static_cast<size_t>(n)] == -7, "no write past the items");
+    std::vector<std::vector<int>> seen(static_cast<size_t>(nseq) * heads);
+    for (int i = 0; i < n; ++i) {
+      const int32_t* r = &items[4 * static_cast<size_t>(i)];
+      int s = -1;
+      for (int j = 0; j < nseq; ++j)
+        if (cu[j] == r[0] && cu[j + 1] - cu[j] == r[1]) s = j;
+      CHECK(s >= 0 && r[3] >= 0 && r[3] < heads && r[2] >= 0 && r[2] < r[1] && r[2] % block == 0, "item fields");
+      if (s >= 0 && r[3] >= 0 && r[3] < heads) seen[static_cast<size_t>(s) * heads + r[3]].push_back(r[2]);
+    }
+    for (int s = 0; s < nseq; ++s)
+      for (int h = 0; h < heads; ++h) {
+        std::vector<int>& t = seen[static_cast<size_t>(s) * heads + h];
+        const int L = cu[s + 1] - cu[s];
+        std::vector<int> want;
+        for (int r0 = 0; r0 < L; r0 += block) want.push_back(r0);
+        std::sort(t.begin(), t.end());
+        CHECK(t == want, "tiles of a (clip, head) are each present once");
+      }
+    for (int slots : {1, 7, 256}) {
+      double ms = -1.0, lb = -1.0;
+      CHECK(t2v_plan_makespan(items.data(), n, block, slots, &ms, &lb) == T2V_OK, "makespan");
+      CHECK(ms >= lb - 1e-9 * (1.0 + lb) && lb >= 0.0, "makespan >= lower bound");
+    }
+  }
+}
+
+// Validation: each rejected input yields the error it should, never a crash.
+static void validation(std::mt19937& rng) {
+  int64_t T = 0, Tk = 0;
+  const std::vector<int32_t> good = {0, 5, 5, 12};
+  CHECK(t2v::validate_shape(good.data(), 3, 2, 128, 0.1f, &T) == T2V_OK && T == 12, "valid shape");
+  const std::vector<int32_t> dec = {0, 5, 4};
+  CHECK(t2v::validate_shape(dec.data(), 2, 2, 128, 0.1f, &T) == T2V_ERR_INVALID_ARG, "decreasing offsets");
+  CHECK(t2v::validate_shape(good.data(), 3, 0, 128, 0.1f, &T) == T2V_ERR_INVALID_ARG, "no heads");
+  CHECK(t2v::validate_shape(good.data(), 3, 2, 96, 0.1f, &T) == T2V_ERR_UNSUPPORTED, "head_dim");
+  CHECK(t2v::validate_shape(good.data(), 3, 2, 128, INFINITY, &T) == T2V_ERR_INVALID_ARG, "scale");
+  CHECK(t2v::validate_shape(nullptr, 3, 2, 128, 0.1f, &T) == T2V_ERR_INVALID_ARG, "null offsets");
+  const std::vector<int32_t> keys = {0, 3, 4, 9};  // sequence 1: a key but no queries
+  CHECK(t2v::validate_shape_qk(good.data(), keys.data(), 3, 2, 64, 0.1f, &T, &Tk) == T2V_ERR_INVALID_ARG,
+        "keys without queries");
+  alignas(64) static char buf[4096];
+  std::vector<t2v::Range> in = {{buf, 1024, "a"}}, out = {{buf + 512, 1024, "b"}};
+  CHECK(t2v::validate_pointers(in, out) == T2V_ERR_INVALID_ARG, "overlap");
+  out = {{buf + 1024, 1024, "b"}};
+  CHECK(t2v::validate_pointers(in, out) == T2V_OK, "disjoint");
+  out = {{buf + 1028, 16, "b"}};
+  CHECK(t2v::validate_pointers(in, out) == T2V_ERR_INVALID_ARG, "misaligned");
+  for (int rep = 0; rep < 200; ++rep) {  // random offsets, some of them invalid
+    const int nseq = std::uniform_int_distribution<int>(0, 30)(rng);
+    std::vector<int32_t> cu = random_cu(rng, nseq, 300);
+    if (nseq > 0 && rep % 4 == 0) cu[1 + rng() % nseq] -= 1000;
+    const int st = t2v::validate_shape(cu.data(), nseq, 1 + rng() % 4, rep % 2 ? 64 : 128, 0.2f, &T);
+    CHECK(st == T2V_OK || st == T2V_ERR_INVALID_ARG, "validation status");
+  }
+}
+
+// Planner: schedules respect precedence and the GPU count; a cycle is refused.
+static void planner(std::mt19937& rng) {
+  const std::vector<int32_t> K = {1, 2, 4, 8};
+  for (int rep = 0; rep < 60; ++rep) {
+    const int n = std::uniform_int_distribution<int>(1, 30)(rng);
+    const int N = std::uniform_int_distribution<int>(1, 16)(rng);
+    std::vector<int32_t> ptr(n + 1, 0), idx;
+    for (int c = 0; c < n; ++c) {
+      for (int p = 0; p < c; ++p)
+        if (rng() % 5 == 0) idx.push_back(p);
+      ptr[c + 1] = static_cast<int32_t>(idx.size());
+    }
+    if (idx.empty()) idx.push_back(0);
+    std::vector<double> lat(static_cast<size_t>(n) * K.size()), mem(lat.size());
+    std::uniform_real_distribution<double> u(0.1, 2.0);
+    for (int c = 0; c < n; ++c)
+      for (size_t j = 0; j < K.size(); ++j) {
+        lat[c * K.size() + j] = u(rng) / K[j] + 0.05 * K[j];
+        mem[c * K.size() + j] = u(rng) / K[j];
+      }
+    std::vector<int32_t> deg(n, 0);
+    std::vector<double> start(n, -1.0);
+    double T = -1.0;
+    const int st = t2v_plan_cascades(n, ptr.data(), idx.data(), static_cast<int>(K.size()), K.data(), lat.data(),
+                                     mem.data(), 2.0, N, 16, 20, 0.05, 2, 1234u + rep, deg.data(), start.data(), &T);
+    CHECK(st == T2V_OK, "plan");
+    if (st != T2V_OK) continue;
+    double tmax = 0.0;
+    std::vector<double> end(n);
+    for (int c = 0; c < n; ++c) {
+      size_t j = 0;
+      while (j < K.size() && K[j] != deg[c]) ++j;
+      CHECK(j < K.size() && deg[c] <= N, "degree in K and <= N");
+      end[c] = start[c] + lat[c * K.size() + (j < K.size() ? j : 0)];
+      tmax = std::max(tmax, end[c]);
+      CHECK(start[c] >= 0.0, "start >= 0");
+    }
+    for (int c = 0; c < n; ++c)
+      for (int e = ptr[c]; e < ptr[c + 1]; ++e) CHECK(start[c] >= end[idx[e]] - 1e-9, "precedence");
+    CHECK(std::fabs(tmax - T) <= 1e-9 * (1.0 + T), "makespan is the last end");
+    for (int c = 0; c < n; ++c) {  // GPUs in use when cascade c starts
+      int used = 0;
+      for (int d = 0; d < n; ++d)
+        if (start[d] <= start[c] + 1e-12 && start[c] < end[d] - 1e-12) used += deg[d];
+      CHECK(used <= N, "at most N GPUs in use");
+    }
+  }
+  const std::vector<int32_t> ptr = {0, 1, 2}, idx = {1, 0};  // 0 <- 1 and 1 <- 0
+  const std::vector<int32_t> deg = {1, 1};
+  const std::vector<double> lat = {1.0, 1.0};
+  std::vector<double> start(2);
+  double T = 0.0;
+  CHECK(t2v_list_schedule(2, ptr.data(), idx.data(), deg.data(), lat.data(), 2, start.data(), &T) ==
+            T2V_ERR_INVALID_ARG, "cycle refused");
+}
+
+int main() {
+  std::mt19937 rng(20260);
+  worklists(rng);
+  validation(rng);
+  planner(rng);
+  std::printf("host sanitizer driver: %d failed checks\n", g_failed);
+  return g_failed;
+}
