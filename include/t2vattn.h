@@ -31,10 +31,22 @@
  * the call that adds one more releases the least recently used, which first
  * waits for that list's device to finish its work.
  *
+ * Tiles. The forward and dQ kernels own 256-query tiles (8 waves, one workgroup per CU),
+ * or 128-query tiles (4 waves, two per CU) when no sequence has more than 512 keys; the two
+ * give bitwise-equal results. The dK/dV kernel owns 128-key tiles and loops over the
+ * sequence's queries; when the costliest such loop exceeds an even share of the work over
+ * the GPU's CUs (few, short key segments against long query segments, as in
+ * cross-attention to text), the loops are cut into pieces of at least 2048 queries whose
+ * fp32 partial sums are kept in dq's memory and added in piece order before the dQ kernel
+ * overwrites dq. Results stay deterministic; they differ from the unsplit order only by
+ * rounding.
+ *
  * Environment. T2V_ORDER=natural schedules tiles in pack order instead of longest clip
- * first (for ablations). T2V_LOG=1 prints one line to stderr per new work list: its items,
- * the host's predicted list-scheduling makespan and its lower bound. T2V_TEST_FAIL_ALLOC=1
- * makes building a new work list fail with T2V_ERR_OOM, for testing that path.
+ * first (for ablations); T2V_QTILE=wide or narrow forces the forward / dQ tile shape and
+ * T2V_SPLIT=off disables the dK/dV loop split (ablations and tests). T2V_LOG=1 prints one
+ * line to stderr per new work list: its items, the host's predicted list-scheduling
+ * makespan and its lower bound, and the loop split if any. T2V_TEST_FAIL_ALLOC=1 makes
+ * building a new work list fail with T2V_ERR_OOM, for testing that path.
  *
  * Threads. Calls from several host threads, on one stream or several, are
  * safe: the cache is guarded by a mutex and a work list stays allocated while
@@ -91,6 +103,7 @@ int t2v_attn_fwd(const void* q, const void* k, const void* v,
  *   out, lse   the forward outputs for the same inputs (device, read only)
  *   dout       device bf16 [T, H, D], the gradient of the loss w.r.t. out
  *   dq, dk, dv device bf16 [T, H, D], written; must not overlap each other or any input
+ *              (dq's memory also serves as scratch during the call, see Tiles above)
  *   delta_ws   device fp32 [2, H, T], caller-owned scratch (8 * H * T bytes): receives
  *              -Delta = -rowsum(dout * out) in [0] and lse * log2(e) in [1]
  *   stream     hipStream_t to launch on

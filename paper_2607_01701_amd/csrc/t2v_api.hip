@@ -30,6 +30,36 @@ int order_from_env() {
   return T2V_ORDER_LONGEST_FIRST;
 }
 
+// Forward / dQ tile shape: narrow (4-wave, two workgroups per CU) when every key segment
+// has at most kNarrowMaxKeys keys, where per-tile loads and stores outweigh the short
+// loop; wide (8-wave) otherwise. T2V_QTILE=wide or narrow forces one (for ablations).
+constexpr int kNarrowMaxKeys = 512;
+
+bool narrow_tiles(const int32_t* cu_k, int nseq) {
+  const char* s = std::getenv("T2V_QTILE");
+  if (s != nullptr && std::strcmp(s, "wide") == 0) return false;
+  if (s != nullptr && std::strcmp(s, "narrow") == 0) return true;
+  for (int i = 0; i < nseq; ++i)
+    if (cu_k[i + 1] - cu_k[i] > kNarrowMaxKeys) return false;
+  return true;
+}
+
+// T2V_SPLIT=off disables the dK/dV loop split (for ablations).
+bool split_enabled() {
+  const char* s = std::getenv("T2V_SPLIT");
+  return s == nullptr || std::strcmp(s, "off") != 0;
+}
+
+int cu_count() {
+  int device = 0, n = 0;
+  if (hipGetDevice(&device) != hipSuccess ||
+      hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  return n;
+}
+
 // T2V_LOG=1: one line on stderr per new work list (items, predicted makespan, bound).
 bool log_enabled() {
   const char* s = std::getenv("T2V_LOG");
@@ -62,10 +92,10 @@ int check_host_pointer(const int32_t* cu) {
 // another thread meanwhile stays alive; the last reference frees it.
 struct Plan {
   std::vector<int32_t> cu, cu_loop;  // offsets of the owned and the looped-over segments
-  int heads = 0, block = 0, order = 0, device = 0;
-  Item* d_items = nullptr;
+  int heads = 0, block = 0, order = 0, device = 0, chunk = 0;
+  Item* d_items = nullptr;  // n_items work items, then n_reduce split tiles (loop split)
   Item* h_items = nullptr;  // pinned source of the upload, kept for the entry's life
-  int n_items = 0;
+  int n_items = 0, n_reduce = 0;
   hipEvent_t ready = nullptr;  // upload finished
   ~Plan() {
     // Launches on any stream may still read d_items: let the plan's device finish first.
@@ -87,8 +117,9 @@ class PlanCache {
  public:
   // Returns the plan (creating and uploading it on `stream` if new) with the
   // upload ordered before any later work on `stream`.
-  int get(const int32_t* cu, const int32_t* cu_loop, int nseq, int heads, int block, int order, hipStream_t stream,
-          PlanRef* out) {
+  // chunk > 0: the loop split of build_worklist, with the reduce list after the items.
+  int get(const int32_t* cu, const int32_t* cu_loop, int nseq, int heads, int block, int order, int chunk,
+          hipStream_t stream, PlanRef* out) {
     int device = 0;
     hipError_t e = hipGetDevice(&device);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
@@ -96,7 +127,7 @@ class PlanCache {
     std::lock_guard<std::mutex> lock(mu_);
     for (auto itr = plans_.begin(); itr != plans_.end(); ++itr) {
       Plan& p = **itr;
-      if (p.heads == heads && p.block == block && p.order == order && p.device == device &&
+      if (p.heads == heads && p.block == block && p.order == order && p.device == device && p.chunk == chunk &&
           p.cu.size() == static_cast<size_t>(nseq + 1) &&
           std::memcmp(p.cu.data(), cu, sizeof(int32_t) * (nseq + 1)) == 0 &&
           std::memcmp(p.cu_loop.data(), cu_loop, sizeof(int32_t) * (nseq + 1)) == 0) {
@@ -114,8 +145,14 @@ class PlanCache {
     p->block = block;
     p->order = order;
     p->device = device;
-    std::vector<Item> items = build_worklist(cu, cu_loop, nseq, heads, block, order);
+    p->chunk = chunk;
+    std::vector<Item> items = build_worklist(cu, cu_loop, nseq, heads, block, order, chunk);
     p->n_items = static_cast<int>(items.size());
+    if (chunk > 0) {
+      const std::vector<Item> red = build_reduce_list(cu, cu_loop, nseq, heads, block, chunk);
+      p->n_reduce = static_cast<int>(red.size());
+      items.insert(items.end(), red.begin(), red.end());
+    }
     const size_t bytes = items.size() * sizeof(Item);
     if (log_enabled()) {
       int ncu = 0;
@@ -124,9 +161,11 @@ class PlanCache {
       plan_makespan(items.data(), p->n_items, block, ncu > 0 ? ncu : 1, &ms, &lb);
       std::fprintf(stderr,
                    "t2v: work list: %d sequences, %d heads, %d-row tiles, %s order: %d items, predicted makespan "
-                   "%.4g (lower bound %.4g, ratio %.4f) on %d CUs\n",
+                   "%.4g (lower bound %.4g, ratio %.4f) on %d CUs",
                    nseq, heads, block, order == T2V_ORDER_NATURAL ? "pack" : "longest-first", p->n_items, ms, lb,
                    lb > 0.0 ? ms / lb : 1.0, ncu);
+      if (chunk > 0) std::fprintf(stderr, "; loops split at %d rows, %d split tiles", chunk, p->n_reduce);
+      std::fprintf(stderr, "\n");
     }
     if (bytes > 0 && fail_alloc_for_test()) return set_error(T2V_ERR_OOM, "hipMalloc of the work list failed (forced)");
     if (bytes > 0) {
@@ -321,9 +360,11 @@ int attn_fwd_impl(const void* q, const void* k, const void* v, const int32_t* cu
     if (int st = check_host_pointer(cu_k)) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   PlanRef plan;
-  if (int st = cache().get(cu_q, cu_k, nseq, heads, fwd_tile_rows(head_dim), order_from_env(), s, &plan)) return st;
+  const int rows = fwd_tile_rows(head_dim, narrow_tiles(cu_k, nseq));
+  if (int st = cache().get(cu_q, cu_k, nseq, heads, rows, order_from_env(), 0, s, &plan)) return st;
   if (plan->n_items == 0) return T2V_OK;
   AttnArgs a{};
+  a.q_rows = rows;
   a.q = q;
   a.k = k;
   a.v = v;
@@ -361,9 +402,20 @@ int attn_bwd_impl(const void* q, const void* k, const void* v, const void* out, 
   const int order = order_from_env();
   PlanRef pk, pq;
   // dK/dV tiles own keys and loop over queries; dQ tiles own queries and loop over keys.
-  if (int st = cache().get(cu_k, cu_q, nseq, heads, dkdv_tile_rows(head_dim), order, s, &pk)) return st;
-  if (int st = cache().get(cu_q, cu_k, nseq, heads, dq_tile_rows(head_dim), order, s, &pq)) return st;
+  // Loops too long for the available parallelism (short keys, long queries) are split into
+  // pieces whose fp32 partial sums go to slots in dq's memory: dq is an output that the dQ
+  // kernel, launched after the reduce, overwrites, so the slots are capped at its size.
+  const int kv_rows = dkdv_tile_rows(head_dim);
+  const int q_rows = dq_tile_rows(head_dim, narrow_tiles(cu_k, nseq));
+  int chunk = 0;
+  if (split_enabled())
+    chunk = choose_loop_split(cu_k, cu_q, nseq, heads, kv_rows, cu_count(), qb / dkdv_partial_slot_bytes(head_dim))
+                .chunk;
+  if (int st = cache().get(cu_k, cu_q, nseq, heads, kv_rows, order, chunk, s, &pk)) return st;
+  if (int st = cache().get(cu_q, cu_k, nseq, heads, q_rows, order, 0, s, &pq)) return st;
   AttnArgs a{};
+  a.q_rows = q_rows;
+  a.partial = static_cast<float*>(dq);
   a.q = q;
   a.k = k;
   a.v = v;
@@ -382,7 +434,11 @@ int attn_bwd_impl(const void* q, const void* k, const void* v, const void* out, 
   if (e != hipSuccess) return hip_fail(e, "backward preprocess launch");
   if (pk->n_items > 0) {
     a.trace = tracer().reserve(pk->n_items);
-    e = timer().run(kSlotDkdv, s, [&] { return launch_bwd_dkdv(a, pk->d_items, pk->n_items, s); });
+    e = timer().run(kSlotDkdv, s, [&] {
+      hipError_t r = launch_bwd_dkdv(a, pk->d_items, pk->n_items, s);
+      if (r == hipSuccess && pk->n_reduce > 0) r = launch_bwd_dkdv_reduce(a, pk->d_items + pk->n_items, pk->n_reduce, s);
+      return r;
+    });
     if (e != hipSuccess) return hip_fail(e, "dK/dV kernel launch");
   }
   if (pq->n_items > 0) {

@@ -10,6 +10,7 @@ namespace {
 
 constexpr int kDkdvBM = 64;     // queries per LDS stage (a multiple of 32)
 constexpr int kDkdvStages = 4;  // LDS stages: up to 3 tiles of Q / dO in flight during one tile's work
+constexpr int kDkdvKeys = (kThreads / 64) * 32;  // keys per workgroup: 32 per wave
 
 // Asynchronous copy of consecutive floats into LDS, one per active lane of the calling
 // wave: lane i copies row i0 + off + i, clamped to L - 1, to lds[i]. The tile's first row
@@ -127,7 +128,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
     const bf16* __restrict__ dout, const float* __restrict__ lse2, const float* __restrict__ ndelta,
     const Item* __restrict__ items, int H, int64_t T, float c, float scale, bf16* __restrict__ dk,
-    bf16* __restrict__ dv, unsigned long long* __restrict__ trace) {
+    bf16* __restrict__ dv, float* __restrict__ partial, unsigned long long* __restrict__ trace) {
   const unsigned long long trace_t0 = trace != nullptr ? trace_clock() : 0ull;
   constexpr int KK = D / 16;
   constexpr int DB = D / 32;
@@ -247,7 +248,23 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
     }
   }
 
-  if (wave_active) {
+  if (wave_active && it.slot >= 0) {
+    // One piece of a split loop: unscaled fp32 sums into the item's partial slot
+    // ([dK | dV] x tile key x head dim), added up in piece order by the reduce kernel.
+    float* pk = partial + static_cast<int64_t>(it.slot) * (2 * kDkdvKeys * D);
+    float* pv = pk + kDkdvKeys * D;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int kr = wave * 32 + (r >> 2) * 8 + G * 4 + (r & 3);  // key within the tile
+      if (it.tile0 + kr < Lk) {
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          pk[kr * D + db * 32 + l32] = dka[db][r];
+          pv[kr * D + db * 32 + l32] = dva[db][r];
+        }
+      }
+    }
+  } else if (wave_active) {
     // Accumulators: lane = head-dim column db*32 + l32, register r = key 8 (r/4) + 4 G + r % 4.
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
@@ -264,9 +281,60 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
   if (trace != nullptr) trace_end(trace, trace_t0, 2);
 }
 
+// Sum of the partial slots of one split tile, in piece order, scaled (dK) and rounded to
+// bf16. A workgroup takes 32 keys of a tile; each thread four consecutive head-dim columns.
+template <int D>
+__global__ __launch_bounds__(kThreads) void dkdv_reduce_kernel(const float* __restrict__ partial,
+                                                               const Item* __restrict__ tiles, int H, float scale,
+                                                               bf16* __restrict__ dk, bf16* __restrict__ dv) {
+  constexpr int kQuarters = kDkdvKeys / 32;
+  constexpr int C4 = D / 4;  // float4 columns per key row
+  const Item it = tiles[blockIdx.x / kQuarters];
+  const int k0 = (blockIdx.x % kQuarters) * 32;  // first key of this block, within the tile
+  const int nkeys = min(32, it.len - it.tile0 - k0);
+  const int64_t rs = static_cast<int64_t>(H) * D;
+  const int64_t slot_elems = 2 * kDkdvKeys * D;
+  for (int e = threadIdx.x; e < 2 * 32 * C4; e += kThreads) {
+    const int which = e / (32 * C4);  // 0: dK, 1: dV
+    const int r = (e / C4) % 32;
+    const int c4 = e % C4;
+    if (r >= nkeys) continue;
+    const float* src = partial + static_cast<int64_t>(it.slot) * slot_elems + which * kDkdvKeys * D +
+                       (k0 + r) * D + c4 * 4;
+    f32x4 acc = *reinterpret_cast<const f32x4*>(src);
+    for (int p = 1; p < it.pieces; ++p) {
+      const f32x4 x = *reinterpret_cast<const f32x4*>(src + p * slot_elems);
+      acc[0] += x[0];
+      acc[1] += x[1];
+      acc[2] += x[2];
+      acc[3] += x[3];
+    }
+    const float m = which == 0 ? scale : 1.0f;
+    bf16x4 w;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) w[i] = static_cast<bf16>(acc[i] * m);
+    bf16* dst = (which == 0 ? dk : dv) + static_cast<int64_t>(it.row0 + it.tile0 + k0 + r) * rs +
+                static_cast<int64_t>(it.head) * D + c4 * 4;
+    *reinterpret_cast<bf16x4*>(dst) = w;
+  }
+}
+
 }  // namespace
 
-int dkdv_tile_rows(int) { return (kThreads / 64) * 32; }
+int dkdv_tile_rows(int) { return kDkdvKeys; }
+
+int64_t dkdv_partial_slot_bytes(int head_dim) { return 2LL * kDkdvKeys * head_dim * 4; }
+
+hipError_t launch_bwd_dkdv_reduce(const AttnArgs& a, const Item* tiles, int n_tiles, hipStream_t stream) {
+  const dim3 grid(n_tiles * (kDkdvKeys / 32)), block(kThreads);
+  auto* dk = static_cast<bf16*>(a.dk);
+  auto* dv = static_cast<bf16*>(a.dv);
+  if (a.head_dim == 128)
+    hipLaunchKernelGGL((dkdv_reduce_kernel<128>), grid, block, 0, stream, a.partial, tiles, a.heads, a.scale, dk, dv);
+  else
+    hipLaunchKernelGGL((dkdv_reduce_kernel<64>), grid, block, 0, stream, a.partial, tiles, a.heads, a.scale, dk, dv);
+  return hipGetLastError();
+}
 
 hipError_t launch_bwd_dkdv(const AttnArgs& a, const Item* items, int n_items, hipStream_t stream) {
   const float c = a.scale * kLog2e;
@@ -280,10 +348,10 @@ hipError_t launch_bwd_dkdv(const AttnArgs& a, const Item* items, int n_items, hi
   const float* lse2 = a.delta + a.total_tokens * a.heads;
   if (a.head_dim == 128)
     hipLaunchKernelGGL((attn_bwd_dkdv_kernel<128>), grid, block, 0, stream, q, k, v, g, lse2, a.delta, items,
-                       a.heads, a.total_tokens, c, a.scale, dk, dv, a.trace);
+                       a.heads, a.total_tokens, c, a.scale, dk, dv, a.partial, a.trace);
   else
     hipLaunchKernelGGL((attn_bwd_dkdv_kernel<64>), grid, block, 0, stream, q, k, v, g, lse2, a.delta, items,
-                       a.heads, a.total_tokens, c, a.scale, dk, dv, a.trace);
+                       a.heads, a.total_tokens, c, a.scale, dk, dv, a.partial, a.trace);
   return hipGetLastError();
 }
 }  // namespace t2v

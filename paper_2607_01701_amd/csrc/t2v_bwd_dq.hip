@@ -10,7 +10,10 @@ namespace {
 
 constexpr int kDqQB = 1;  // 32-query blocks per wave
 constexpr int kDqBN = 64; // keys per LDS stage (a multiple of 32)
-constexpr int kDqThreads = 512;  // eight waves (256 queries) share each staged K/V tile
+// Wide tiles: eight waves (256 queries) share each staged K/V tile; narrow tiles: four
+// waves (128 queries), two workgroups per CU, for packs with short key segments.
+constexpr int kDqThreadsWide = 512;
+constexpr int kDqThreadsNarrow = 256;
 
 // ------------------------------------------------------------------------ backward: dQ
 
@@ -80,8 +83,8 @@ T2V_DEV void dq_step(uint32_t kbase, uint32_t vbase, uint32_t kr0, uint32_t kr1,
       for (int qb = 0; qb < QB; ++qb) dqa[qb][db] = mfma(kt[hf][db], sb[qb][hf], dqa[qb][db]);
 }
 
-template <int D, int QB>
-__global__ __launch_bounds__(kDqThreads, 1) void attn_bwd_dq_kernel(
+template <int D, int QB, int NT>
+__global__ __launch_bounds__(NT, 512 / NT) void attn_bwd_dq_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
     const bf16* __restrict__ dout, const float* __restrict__ lse2, const float* __restrict__ ndelta,
     const Item* __restrict__ items, int H, int64_t T, float c, float scale, bf16* __restrict__ dq,
@@ -110,7 +113,7 @@ __global__ __launch_bounds__(kDqThreads, 1) void attn_bwd_dq_kernel(
   const int q_wave0 = it.tile0 + wave * QB * 32;
   const bool wave_active = q_wave0 < Lq;
 
-  const TileDma<D, BN, kDqThreads> dma(tid, rs);
+  const TileDma<D, BN, NT> dma(tid, rs);
   dma.copy(sK[0], kh, rs, 0, L);
   dma.copy(sV[0], vh, rs, 0, L);
 
@@ -194,23 +197,37 @@ __global__ __launch_bounds__(kDqThreads, 1) void attn_bwd_dq_kernel(
 
 }  // namespace
 
-int dq_tile_rows(int) { return (kDqThreads / 64) * 32 * kDqQB; }
+int dq_tile_rows(int, bool narrow) { return ((narrow ? kDqThreadsNarrow : kDqThreadsWide) / 64) * 32 * kDqQB; }
 
-hipError_t launch_bwd_dq(const AttnArgs& a, const Item* items, int n_items, hipStream_t stream) {
+namespace {
+template <int D, int NT>
+void launch_dq_as(const AttnArgs& a, const Item* items, int n_items, hipStream_t stream) {
   const float c = a.scale * kLog2e;
-  const dim3 grid(n_items), block(kDqThreads);
   const auto* q = static_cast<const bf16*>(a.q);
   const auto* k = static_cast<const bf16*>(a.k);
   const auto* v = static_cast<const bf16*>(a.v);
   const auto* g = static_cast<const bf16*>(a.dout);
   auto* dq = static_cast<bf16*>(a.dq);
   const float* lse2 = a.delta + a.total_tokens * a.heads;
-  if (a.head_dim == 128)
-    hipLaunchKernelGGL((attn_bwd_dq_kernel<128, kDqQB>), grid, block, 0, stream, q, k, v, g, lse2, a.delta,
-                       items, a.heads, a.total_tokens, c, a.scale, dq, a.trace);
-  else
-    hipLaunchKernelGGL((attn_bwd_dq_kernel<64, kDqQB>), grid, block, 0, stream, q, k, v, g, lse2, a.delta,
-                       items, a.heads, a.total_tokens, c, a.scale, dq, a.trace);
+  hipLaunchKernelGGL((attn_bwd_dq_kernel<D, kDqQB, NT>), dim3(n_items), dim3(NT), 0, stream, q, k, v, g, lse2,
+                     a.delta, items, a.heads, a.total_tokens, c, a.scale, dq, a.trace);
+}
+}  // namespace
+
+hipError_t launch_bwd_dq(const AttnArgs& a, const Item* items, int n_items, hipStream_t stream) {
+  const bool narrow = a.q_rows == dq_tile_rows(a.head_dim, true);
+  if (!narrow && a.q_rows != dq_tile_rows(a.head_dim, false)) return hipErrorInvalidValue;
+  if (a.head_dim == 128) {
+    if (narrow)
+      launch_dq_as<128, kDqThreadsNarrow>(a, items, n_items, stream);
+    else
+      launch_dq_as<128, kDqThreadsWide>(a, items, n_items, stream);
+  } else {
+    if (narrow)
+      launch_dq_as<64, kDqThreadsNarrow>(a, items, n_items, stream);
+    else
+      launch_dq_as<64, kDqThreadsWide>(a, items, n_items, stream);
+  }
   return hipGetLastError();
 }
 }  // namespace t2v

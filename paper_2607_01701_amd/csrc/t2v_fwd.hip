@@ -30,10 +30,13 @@ namespace {
 
 constexpr int kFwdQB = 1;  // 32-query blocks per wave
 constexpr int kFwdBN = 64; // keys per LDS stage (a multiple of 32)
-// Eight waves (two per SIMD, 256 queries) share each staged K/V tile, so every tile crosses
-// from L2 into LDS once per 256 queries rather than once per 128 (measured: forward +3-5%
-// against two independent 4-wave workgroups per CU).
-constexpr int kFwdThreads = 512;
+// Wide tiles: eight waves (two per SIMD, 256 queries) share each staged K/V tile, so every
+// tile crosses from L2 into LDS once per 256 queries rather than once per 128 (measured:
+// forward +3-5% against two independent 4-wave workgroups per CU on long clips). Narrow
+// tiles: four waves (128 queries), two workgroups per CU, for packs whose key segments are
+// short: there one workgroup's Q loads and O stores overlap the other's MFMA work.
+constexpr int kFwdThreadsWide = 512;
+constexpr int kFwdThreadsNarrow = 256;
 
 // ------------------------------------------------------------------------------ forward
 
@@ -139,8 +142,8 @@ T2V_DEV void fwd_step(uint32_t kbase, uint32_t vbase0, uint32_t vbase1, int kb, 
   }
 }
 
-template <int D, int QB, bool NEG>
-__global__ __launch_bounds__(kFwdThreads, 1) void attn_fwd_kernel(
+template <int D, int QB, bool NEG, int NT>
+__global__ __launch_bounds__(NT, 512 / NT) void attn_fwd_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
     const Item* __restrict__ items, int H, int64_t T, float c, bf16* __restrict__ out,
     float* __restrict__ lse, unsigned long long* __restrict__ trace) {
@@ -167,7 +170,7 @@ __global__ __launch_bounds__(kFwdThreads, 1) void attn_fwd_kernel(
   const int q_wave0 = it.tile0 + wave * QB * 32;
   const bool wave_active = q_wave0 < Lq;
 
-  const TileDma<D, BN, kFwdThreads> dma(tid, rs);
+  const TileDma<D, BN, NT> dma(tid, rs);
   dma.copy(sK[0], kh, rs, 0, L);
   dma.copy(sV[0], vh, rs, 0, L);
 
@@ -253,31 +256,46 @@ __global__ __launch_bounds__(kFwdThreads, 1) void attn_fwd_kernel(
 
 }  // namespace
 
-int fwd_tile_rows(int) { return (kFwdThreads / 64) * 32 * kFwdQB; }
+int fwd_tile_rows(int, bool narrow) { return ((narrow ? kFwdThreadsNarrow : kFwdThreadsWide) / 64) * 32 * kFwdQB; }
+
+namespace {
+template <int D, bool NEG, int NT>
+void launch_fwd_as(const AttnArgs& a, const bf16* q, const bf16* k, const bf16* v, bf16* o, float* lse,
+                   const Item* items, int n_items, float c, hipStream_t stream) {
+  hipLaunchKernelGGL((attn_fwd_kernel<D, kFwdQB, NEG, NT>), dim3(n_items), dim3(NT), 0, stream, q, k, v, items,
+                     a.heads, a.total_tokens, c, o, lse, a.trace);
+}
+
+template <int D, bool NEG>
+void launch_fwd_d(const AttnArgs& a, const bf16* q, const bf16* k, const bf16* v, bf16* o, float* lse,
+                  const Item* items, int n_items, float c, hipStream_t stream) {
+  if (a.q_rows == fwd_tile_rows(D, true))
+    launch_fwd_as<D, NEG, kFwdThreadsNarrow>(a, q, k, v, o, lse, items, n_items, c, stream);
+  else
+    launch_fwd_as<D, NEG, kFwdThreadsWide>(a, q, k, v, o, lse, items, n_items, c, stream);
+}
+}  // namespace
 
 hipError_t launch_fwd(const AttnArgs& a, void* out, float* lse, const Item* items, int n_items,
                       hipStream_t stream) {
+  if (a.q_rows != fwd_tile_rows(a.head_dim, true) && a.q_rows != fwd_tile_rows(a.head_dim, false))
+    return hipErrorInvalidValue;
   const float c = a.scale * kLog2e;
   const auto* q = static_cast<const bf16*>(a.q);
   const auto* k = static_cast<const bf16*>(a.k);
   const auto* v = static_cast<const bf16*>(a.v);
   auto* o = static_cast<bf16*>(out);
-  const dim3 grid(n_items), block(kFwdThreads);
   const bool neg = a.scale < 0.0f;
   if (a.head_dim == 128) {
     if (neg)
-      hipLaunchKernelGGL((attn_fwd_kernel<128, kFwdQB, true>), grid, block, 0, stream, q, k, v, items, a.heads,
-                         a.total_tokens, c, o, lse, a.trace);
+      launch_fwd_d<128, true>(a, q, k, v, o, lse, items, n_items, c, stream);
     else
-      hipLaunchKernelGGL((attn_fwd_kernel<128, kFwdQB, false>), grid, block, 0, stream, q, k, v, items, a.heads,
-                         a.total_tokens, c, o, lse, a.trace);
+      launch_fwd_d<128, false>(a, q, k, v, o, lse, items, n_items, c, stream);
   } else {
     if (neg)
-      hipLaunchKernelGGL((attn_fwd_kernel<64, kFwdQB, true>), grid, block, 0, stream, q, k, v, items, a.heads,
-                         a.total_tokens, c, o, lse, a.trace);
+      launch_fwd_d<64, true>(a, q, k, v, o, lse, items, n_items, c, stream);
     else
-      hipLaunchKernelGGL((attn_fwd_kernel<64, kFwdQB, false>), grid, block, 0, stream, q, k, v, items, a.heads,
-                         a.total_tokens, c, o, lse, a.trace);
+      launch_fwd_d<64, false>(a, q, k, v, o, lse, items, n_items, c, stream);
   }
   return hipGetLastError();
 }

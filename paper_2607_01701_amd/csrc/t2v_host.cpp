@@ -99,34 +99,103 @@ int validate_pointers(const std::vector<Range>& inputs, const std::vector<Range>
 
 namespace {
 
+// The tiles of one (sequence, head), or of one piece of its loop when the loop is split.
 struct Group {
   int seq, head;
   int32_t row0, len;    // owned segment
-  int32_t lrow0, llen;  // looped-over segment
+  int32_t lrow0, llen;  // looped-over segment (or piece)
   int tiles;
+  int32_t slot0 = -1;   // first partial slot of the (sequence, head); -1: not split
+  int piece = 0, pieces = 1;
 };
 
-std::vector<Group> make_groups(const int32_t* cu, const int32_t* cul, int nseq, int heads, int block) {
+std::vector<Group> make_groups(const int32_t* cu, const int32_t* cul, int nseq, int heads, int block, int chunk) {
   std::vector<Group> g;
+  int64_t next_slot = 0;
   for (int s = 0; s < nseq; ++s) {
     const int32_t L = cu[s + 1] - cu[s];
     const int32_t LL = cul[s + 1] - cul[s];
     if (L <= 0 || LL <= 0) continue;
     const int tiles = (L + block - 1) / block;
-    for (int h = 0; h < heads; ++h) g.push_back({s, h, cu[s], L, cul[s], LL, tiles});
+    int n = 1, step = LL;
+    loop_pieces(LL, chunk, &n, &step);
+    for (int h = 0; h < heads; ++h) {
+      if (n == 1) {
+        g.push_back({s, h, cu[s], L, cul[s], LL, tiles});
+        continue;
+      }
+      const auto slot0 = static_cast<int32_t>(next_slot);
+      next_slot += static_cast<int64_t>(tiles) * n;
+      for (int j = 0; j < n; ++j)
+        g.push_back({s, h, cu[s], L, cul[s] + j * step, std::min(step, LL - j * step), tiles, slot0, j, n});
+    }
   }
   return g;
 }
 
 void append_tiles(std::vector<Item>& out, const Group& g, int t_begin, int t_end, int block) {
-  for (int t = t_begin; t < t_end; ++t) out.push_back({g.row0, g.len, t * block, g.head, g.lrow0, g.llen, 0, 0});
+  for (int t = t_begin; t < t_end; ++t) {
+    const int32_t slot = g.pieces > 1 ? g.slot0 + t * g.pieces + g.piece : -1;
+    out.push_back({g.row0, g.len, t * block, g.head, g.lrow0, g.llen, slot, g.pieces});
+  }
 }
 
 }  // namespace
 
+void loop_pieces(int LL, int chunk, int* n, int* step) {
+  *n = 1;
+  *step = LL;
+  if (chunk <= 0 || LL <= chunk) return;
+  const int n0 = (LL + chunk - 1) / chunk;
+  const int s = ((LL + n0 - 1) / n0 + 63) / 64 * 64;
+  const int n1 = (LL + s - 1) / s;
+  if (n1 <= 1) return;
+  *n = n1;
+  *step = s;
+}
+
+LoopSplit choose_loop_split(const int32_t* cu, const int32_t* cul, int nseq, int heads, int block, int parallel,
+                            int64_t max_slots) {
+  double total = 0.0, largest = 0.0;
+  int32_t longest = 0;
+  for (int s = 0; s < nseq; ++s) {
+    const int32_t L = cu[s + 1] - cu[s], LL = cul[s + 1] - cul[s];
+    if (L <= 0 || LL <= 0) continue;
+    total += static_cast<double>(heads) * L * LL;
+    largest = std::max(largest, static_cast<double>(std::min(block, L)) * LL);
+    longest = std::max(longest, LL);
+  }
+  if (parallel < 1 || block < 1 || largest <= total / parallel) return {};
+  const double share = std::ceil(total / (2.0 * parallel * block));
+  int64_t chunk = std::max<int64_t>(kMinChunk, (static_cast<int64_t>(share) + 63) / 64 * 64);
+  for (; chunk < longest; chunk *= 2) {  // widen the pieces until their partial slots fit
+    int64_t slots = 0;
+    for (int s = 0; s < nseq; ++s) {
+      const int32_t L = cu[s + 1] - cu[s], LL = cul[s + 1] - cul[s];
+      if (L <= 0 || LL <= 0) continue;
+      int n = 1, step = LL;
+      loop_pieces(LL, static_cast<int>(chunk), &n, &step);
+      if (n > 1) slots += static_cast<int64_t>(heads) * ((L + block - 1) / block) * n;
+    }
+    if (slots == 0) return {};
+    if (slots <= max_slots && slots <= INT32_MAX) return {static_cast<int>(chunk), slots};
+  }
+  return {};
+}
+
+std::vector<Item> build_reduce_list(const int32_t* cu, const int32_t* cul, int nseq, int heads, int block,
+                                    int chunk) {
+  std::vector<Item> out;
+  for (const Group& g : make_groups(cu, cul, nseq, heads, block, chunk))
+    if (g.pieces > 1 && g.piece == 0)
+      for (int t = 0; t < g.tiles; ++t)
+        out.push_back({g.row0, g.len, t * block, g.head, 0, 0, g.slot0 + t * g.pieces, g.pieces});
+  return out;
+}
+
 std::vector<Item> build_worklist(const int32_t* cu, const int32_t* cu_loop, int nseq, int heads, int block,
-                                 int order) {
-  std::vector<Group> groups = make_groups(cu, cu_loop, nseq, heads, block);
+                                 int order, int chunk) {
+  std::vector<Group> groups = make_groups(cu, cu_loop, nseq, heads, block, chunk);
   std::vector<Item> items;
   size_t n = 0;
   for (const auto& g : groups) n += g.tiles;
@@ -242,7 +311,7 @@ int t2v_plan_makespan(const int32_t* items, int n_items, int block, int slots, d
   std::vector<t2v::Item> it(static_cast<size_t>(n_items));
   for (int i = 0; i < n_items; ++i) {  // self-attention items: the loop segment is the clip
     const int32_t* r = items + 4 * static_cast<size_t>(i);
-    it[i] = {r[0], r[1], r[2], r[3], r[0], r[1], 0, 0};
+    it[i] = {r[0], r[1], r[2], r[3], r[0], r[1], -1, 1};
   }
   t2v::plan_makespan(it.data(), n_items, block, slots, makespan_out, lower_bound_out);
   return T2V_OK;

@@ -20,7 +20,12 @@ struct Item {
   int32_t head;   // head index
   int32_t lrow0;  // first row of the looped-over segment in its packed tensor
   int32_t llen;   // looped-over segment length (>= 1 whenever len >= 1)
-  int32_t pad0, pad1;
+  // Loop split (dK/dV only): when the looped-over segment is cut into `pieces` > 1 pieces,
+  // the item covers one piece (lrow0 / llen describe the piece) and writes fp32 partial
+  // sums to partial slot `slot`; otherwise slot = -1 and pieces = 1. In a reduce list the
+  // item is one split tile, slot its first slot and pieces the slot count.
+  int32_t slot;
+  int32_t pieces;
 };
 static_assert(sizeof(Item) == 32, "Item is one 256-bit scalar load");
 
@@ -49,9 +54,35 @@ int validate_shape_qk(const int32_t* cu_q, const int32_t* cu_k, int nseq, int he
 
 // Builds the work list for tiles of `block` rows of the owned segments (offsets cu_own),
 // each looping over the matching segment of cu_loop (see t2v_build_worklist in t2vattn.h;
-// self-attention passes the same offsets twice).
+// self-attention passes the same offsets twice). chunk > 0 cuts every looped-over segment
+// longer than chunk rows into pieces (loop_pieces), one item per tile and piece; the
+// partial slot of (sequence s, head h, tile t, piece j) is base(s, h) + t * pieces + j, with
+// base counted over the split (sequence, head) pairs in pack order.
 std::vector<Item> build_worklist(const int32_t* cu_own, const int32_t* cu_loop, int nseq, int heads, int block,
-                                 int order);
+                                 int order, int chunk = 0);
+
+// Pieces of a loop of LL rows cut at chunk rows: *n pieces of *step rows (a multiple of
+// 64), the last taking the rest. *n = 1 (step = LL) when chunk <= 0 or LL <= chunk.
+void loop_pieces(int LL, int chunk, int* n, int* step);
+
+// Loop split of a work list (used for dK/dV, whose loop over a long query segment is the
+// critical path when few key tiles exist, as in cross-attention against short text).
+struct LoopSplit {
+  int chunk = 0;       // rows per piece before rounding; 0: no split
+  int64_t slots = 0;   // partial slots the pieces write
+};
+constexpr int kMinChunk = 2048;  // smallest piece: keeps the partial traffic small against the work
+
+// No split unless the costliest tile (rows x loop length) exceeds an even share of all work
+// over `parallel` workers; then pieces near an even share over 2 x parallel, at least
+// kMinChunk rows, widened until the partial slots fit in max_slots.
+LoopSplit choose_loop_split(const int32_t* cu_own, const int32_t* cu_loop, int nseq, int heads, int block,
+                            int parallel, int64_t max_slots);
+
+// One item per split tile of build_worklist(..., chunk): row0, len, tile0, head of the tile,
+// slot = its first partial slot, pieces = the number of consecutive slots to sum.
+std::vector<Item> build_reduce_list(const int32_t* cu_own, const int32_t* cu_loop, int nseq, int heads, int block,
+                                    int chunk);
 
 // Greedy list-scheduling makespan of `items` on `slots` workers, dealt per XCD when
 // slots is a multiple of kNumXcd. Costs are tile rows x looped-over length.

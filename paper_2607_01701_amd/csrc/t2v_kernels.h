@@ -9,10 +9,13 @@
 
 namespace t2v {
 
-// Rows per work item of each kernel (the tile sizes the scheduler cuts clips into).
-int fwd_tile_rows(int head_dim);
+// Rows per work item of each kernel (the tile sizes the scheduler cuts clips into). The
+// forward and dQ kernels come in a wide (8-wave) and a narrow (4-wave) form.
+int fwd_tile_rows(int head_dim, bool narrow);
 int dkdv_tile_rows(int head_dim);
-int dq_tile_rows(int head_dim);
+int dq_tile_rows(int head_dim, bool narrow);
+// Bytes of one dK/dV partial slot (fp32 dK and dV of one tile of keys).
+int64_t dkdv_partial_slot_bytes(int head_dim);
 
 struct AttnArgs {
   const void* q;
@@ -31,12 +34,15 @@ struct AttnArgs {
   float scale;
   // Per-workgroup trace records of the launch being made (4 uint64 each), or nullptr.
   unsigned long long* trace = nullptr;
+  int q_rows = 0;            // forward / dQ tile rows: selects the wide or narrow kernels
+  float* partial = nullptr;  // dK/dV partial slots of split loops (work items with slot >= 0)
 };
 
 hipError_t launch_fwd(const AttnArgs& a, void* out, float* lse, const Item* items, int n_items,
                       hipStream_t stream);
 hipError_t launch_bwd_pre(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_bwd_dkdv(const AttnArgs& a, const Item* items, int n_items, hipStream_t stream);
+hipError_t launch_bwd_dkdv_reduce(const AttnArgs& a, const Item* tiles, int n_tiles, hipStream_t stream);
 hipError_t launch_bwd_dq(const AttnArgs& a, const Item* items, int n_items, hipStream_t stream);
 
 }  // namespace t2v

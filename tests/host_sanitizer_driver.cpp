@@ -1,5 +1,5 @@
-// Randomised exercise of the host-side code of libt2vattn (tile scheduler, makespan model,
-// argument validation, cascade planner), built with AddressSanitizer and
+// Randomised exercise of the host-side code of libt2vattn (tile scheduler and its loop
+// split, makespan model, argument validation, cascade planner), built with AddressSanitizer and
 // UndefinedBehaviorSanitizer by tests/test_host_sanitizers.py. Every check that fails prints
 // a line; the exit status is the number of failed checks (sanitizer reports abort earlier).
 #include <algorithm>
@@ -75,6 +75,91 @@ static void worklists(std::mt19937& rng) {
       CHECK(ms >= lb - 1e-9 * (1.0 + lb) && lb >= 0.0, "makespan >= lower bound");
     }
   }
+}
+
+// Loop split: every (sequence, head, tile) loop is covered once by its pieces, pieces are
+// 64-row multiples but the last, partial slots are unique and consecutive per split tile
+// as its reduce item says, and the chosen split respects its slot cap.
+static void loop_split(std::mt19937& rng) {
+  int chosen = 0;
+  for (int rep = 0; rep < 400; ++rep) {
+    const int LL = std::uniform_int_distribution<int>(1, 50000)(rng);
+    const int chunk = std::uniform_int_distribution<int>(-1, 9000)(rng);
+    int n = 0, step = 0;
+    t2v::loop_pieces(LL, chunk, &n, &step);
+    const bool none = chunk <= 0 || LL <= chunk;
+    CHECK(n >= 1 && (n == 1) == (step == LL), "pieces");
+    CHECK(!none || n == 1, "no split at or below the chunk");
+    CHECK(n == 1 || (step % 64 == 0 && static_cast<int64_t>(n - 1) * step < LL &&
+                     static_cast<int64_t>(n) * step >= LL), "pieces cover the loop");
+  }
+  for (int rep = 0; rep < 200; ++rep) {
+    const int nseq = std::uniform_int_distribution<int>(1, 12)(rng);
+    const int heads = std::uniform_int_distribution<int>(1, 4)(rng);
+    const int block = 128;
+    const std::vector<int32_t> own = random_cu(rng, nseq, 400), loop0 = random_cu(rng, nseq, 30000);
+    std::vector<int32_t> loop(loop0);  // sequences with keys but no queries get one query
+    for (int s = 0, add = 0; s < nseq; ++s) {
+      if (own[s + 1] > own[s] && loop0[s + 1] == loop0[s]) ++add;
+      loop[s + 1] = loop0[s + 1] + add;
+    }
+    const int parallel = rep % 3 == 0 ? 1 : 256;
+    const int64_t cap = rep % 4 == 0 ? 7 : 1 << 20;
+    const t2v::LoopSplit sp = t2v::choose_loop_split(own.data(), loop.data(), nseq, heads, block, parallel, cap);
+    CHECK(sp.chunk == 0 || (sp.chunk >= t2v::kMinChunk && sp.slots >= 2 && sp.slots <= cap), "split choice");
+    CHECK(parallel > 1 || sp.chunk == 0, "one worker: no split");
+    chosen += sp.chunk > 0 ? 1 : 0;
+    const int chunk = sp.chunk > 0 ? sp.chunk : (rep % 2 ? 2048 : 0);
+    const std::vector<t2v::Item> items =
+        t2v::build_worklist(own.data(), loop.data(), nseq, heads, block, T2V_ORDER_LONGEST_FIRST, chunk);
+    const std::vector<t2v::Item> red = t2v::build_reduce_list(own.data(), loop.data(), nseq, heads, block, chunk);
+    int64_t slots = 0;
+    for (const auto& r : red) slots += r.pieces;
+    if (sp.chunk > 0) CHECK(slots == sp.slots, "slot count matches the choice");
+    std::vector<int> slot_seen(static_cast<size_t>(slots), 0);
+    for (const auto& it : items) {
+      CHECK(it.llen >= 1, "piece has rows");
+      if (it.slot >= 0) {
+        CHECK(it.slot < slots && it.pieces >= 2, "slot in range");
+        if (it.slot < slots) ++slot_seen[static_cast<size_t>(it.slot)];
+      } else {
+        CHECK(it.pieces == 1, "unsplit item");
+      }
+    }
+    for (int v : slot_seen) CHECK(v == 1, "every slot written by one item");
+    for (int s = 0; s < nseq; ++s) {
+      const int L = own[s + 1] - own[s], LL = loop[s + 1] - loop[s];
+      if (L <= 0 || LL <= 0) continue;
+      for (int h = 0; h < heads; ++h)
+        for (int t0 = 0; t0 < L; t0 += block) {
+          std::vector<std::pair<int, int>> ranges;
+          std::vector<int32_t> tslots;
+          for (const auto& it : items)
+            if (it.row0 == own[s] && it.len == L && it.head == h && it.tile0 == t0) {
+              ranges.push_back({it.lrow0, it.llen});
+              tslots.push_back(it.slot);
+            }
+          std::sort(ranges.begin(), ranges.end());
+          std::sort(tslots.begin(), tslots.end());
+          int64_t at = loop[s];
+          for (const auto& r : ranges) {
+            CHECK(r.first == at, "pieces are contiguous");
+            at = static_cast<int64_t>(r.first) + r.second;
+          }
+          CHECK(at == loop[s + 1], "pieces end at the loop end");
+          int nr = 0;
+          for (const auto& r : red)
+            if (r.row0 == own[s] && r.head == h && r.tile0 == t0) {
+              ++nr;
+              CHECK(r.pieces == static_cast<int>(ranges.size()) && tslots.front() == r.slot &&
+                        tslots.back() == r.slot + r.pieces - 1, "reduce item names the tile's slots");
+            }
+          CHECK(nr == (ranges.size() > 1 ? 1 : 0), "one reduce item per split tile");
+        }
+    }
+  }
+  std::printf("loop split chosen in %d of 200 packs\n", chosen);
+  CHECK(chosen >= 20, "the random packs exercise the split");
 }
 
 // Validation: each rejected input yields the error it should, never a crash.
@@ -166,6 +251,7 @@ static void planner(std::mt19937& rng) {
 int main() {
   std::mt19937 rng(20260);
   worklists(rng);
+  loop_split(rng);
   validation(rng);
   planner(rng);
   std::printf("host sanitizer driver: %d failed checks\n", g_failed);

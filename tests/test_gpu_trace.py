@@ -55,7 +55,7 @@ def test_trace_records_and_results():
 
 def test_trace_overflow_runs_untraced():
     import torch
-    pack = make_pack([300, 40], 2, 64, seed=71)
+    pack = make_pack([700, 40], 2, 64, seed=71)  # keys > 512: wide (256-row) forward tiles
     dev = dev_inputs(pack)
     nf = n_items(pack, 256)
     rec = torch.zeros(4 * nf, dtype=torch.int64, device="cuda")
