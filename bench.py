@@ -566,8 +566,12 @@ def balance_report(workload: str = "hetero", seed: int = 0):
              "(max(total / slots, largest item)) for the same work list.", "",
              f"{'order':14s} {'kernel':9s} {'WGs':>6s} {'CUs':>4s} {'span ms':>8s} {'busy mean ms':>12s} "
              f"{'CV':>6s} {'idle':>6s} {'host LPT':>9s}"]
+    # Wide forward / dQ tiles and no dK/dV loop split (what the heterogeneous mix uses by
+    # default), so that t2v_build_worklist reproduces the traced work lists.
     rows = {"fwd": 256, "bwd_dkdv": 128, "bwd_dq": 256}
     names = {0: "fwd", 2: "bwd_dkdv", 3: "bwd_dq"}
+    os.environ["T2V_QTILE"], os.environ["T2V_SPLIT"] = "wide", "off"
+    lines.insert(-2, "Tiles: 256 queries (forward, dQ), 128 keys (dK/dV), no loop split.")
     for order in ("longest_first", "natural"):
         os.environ["T2V_ORDER"] = order
         _lib.attn_fwd(q, k, v, pack.cu_seqlens, pack.scale)  # builds and caches the work lists
@@ -602,7 +606,8 @@ def balance_report(workload: str = "hetero", seed: int = 0):
             lines.append(f"{order:14s} {name:9s} {x.shape[0]:6d} {len(busy):4d} {span * 1e-5:8.3f} "
                          f"{b.mean() * 1e-5:12.3f} {b.std() / b.mean():6.3f} {1 - b.sum() / (ncu * span):6.1%} "
                          f"{mk / lb:9.3f}")
-    os.environ.pop("T2V_ORDER", None)
+    for var in ("T2V_ORDER", "T2V_QTILE", "T2V_SPLIT"):
+        os.environ.pop(var, None)
     lines += ["", "(device clock 100 MHz: 1 tick = 10 ns)"]
     return "\n".join(lines)
 

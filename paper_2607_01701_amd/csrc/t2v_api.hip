@@ -30,18 +30,29 @@ int order_from_env() {
   return T2V_ORDER_LONGEST_FIRST;
 }
 
-// Forward / dQ tile shape: narrow (4-wave, two workgroups per CU) when every key segment
-// has at most kNarrowMaxKeys keys, where per-tile loads and stores outweigh the short
-// loop; wide (8-wave) otherwise. T2V_QTILE=wide or narrow forces one (for ablations).
-constexpr int kNarrowMaxKeys = 512;
+// Forward / dQ tile shape: narrow (4 waves, 128 queries) or wide (8 waves, 256 queries).
+// Narrow tiles fit two workgroups per CU at D = 128 and three at D = 64, so one workgroup's
+// Q loads and output stores overlap another's MFMA work; wide tiles stage each K/V tile
+// once per 256 queries. Measured on MI355X (uniform packs): at D = 64 narrow is faster at
+// every length (8-19% forward, 4-12% dQ); at D = 128 the forward crosses over near 1,536
+// keys and dQ near 8,192-16,384. The length compared is the work-weighted key length
+// sum(Lq Lk^2) / sum(Lq Lk), so a mixed pack goes by the clips that dominate its time.
+// T2V_QTILE=wide or narrow forces one (ablations and tests).
+constexpr double kNarrowFwdKeys = 1536.0;
+constexpr double kNarrowDqKeys = 8192.0;
 
-bool narrow_tiles(const int32_t* cu_k, int nseq) {
+bool narrow_tiles(const int32_t* cu_q, const int32_t* cu_k, int nseq, int head_dim, double max_keys) {
   const char* s = std::getenv("T2V_QTILE");
   if (s != nullptr && std::strcmp(s, "wide") == 0) return false;
   if (s != nullptr && std::strcmp(s, "narrow") == 0) return true;
-  for (int i = 0; i < nseq; ++i)
-    if (cu_k[i + 1] - cu_k[i] > kNarrowMaxKeys) return false;
-  return true;
+  if (head_dim == 64) return true;
+  double work = 0.0, weighted = 0.0;
+  for (int i = 0; i < nseq; ++i) {
+    const double lq = cu_q[i + 1] - cu_q[i], lk = cu_k[i + 1] - cu_k[i];
+    work += lq * lk;
+    weighted += lq * lk * lk;
+  }
+  return work <= 0.0 || weighted <= max_keys * work;
 }
 
 // T2V_SPLIT=off disables the dK/dV loop split (for ablations).
@@ -360,7 +371,7 @@ int attn_fwd_impl(const void* q, const void* k, const void* v, const int32_t* cu
     if (int st = check_host_pointer(cu_k)) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   PlanRef plan;
-  const int rows = fwd_tile_rows(head_dim, narrow_tiles(cu_k, nseq));
+  const int rows = fwd_tile_rows(head_dim, narrow_tiles(cu_q, cu_k, nseq, head_dim, kNarrowFwdKeys));
   if (int st = cache().get(cu_q, cu_k, nseq, heads, rows, order_from_env(), 0, s, &plan)) return st;
   if (plan->n_items == 0) return T2V_OK;
   AttnArgs a{};
@@ -406,7 +417,7 @@ int attn_bwd_impl(const void* q, const void* k, const void* v, const void* out, 
   // pieces whose fp32 partial sums go to slots in dq's memory: dq is an output that the dQ
   // kernel, launched after the reduce, overwrites, so the slots are capped at its size.
   const int kv_rows = dkdv_tile_rows(head_dim);
-  const int q_rows = dq_tile_rows(head_dim, narrow_tiles(cu_k, nseq));
+  const int q_rows = dq_tile_rows(head_dim, narrow_tiles(cu_q, cu_k, nseq, head_dim, kNarrowDqKeys));
   int chunk = 0;
   if (split_enabled())
     chunk = choose_loop_split(cu_k, cu_q, nseq, heads, kv_rows, cu_count(), qb / dkdv_partial_slot_bytes(head_dim))

@@ -85,6 +85,7 @@ def test_log_prints_the_plan_summary(monkeypatch, capfd):
     import torch
     from paper_2607_01701_amd import attn_fwd
     monkeypatch.setenv("T2V_LOG", "1")
+    monkeypatch.setenv("T2V_QTILE", "wide")  # 256-row forward tiles
     pack = make_pack([777, 41], 2, 64, seed=90)  # lengths no other test uses: a new work list
     d = dev_inputs(pack)
     attn_fwd(d["q"], d["k"], d["v"], pack.cu_seqlens, pack.scale)

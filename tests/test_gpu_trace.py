@@ -23,8 +23,9 @@ def n_items(pack, rows):
     return _lib.t2v_build_worklist(pack.cu_seqlens, pack.heads, rows).shape[0]
 
 
-def test_trace_records_and_results():
+def test_trace_records_and_results(monkeypatch):
     import torch
+    monkeypatch.setenv("T2V_QTILE", "wide")  # 256-row forward and dQ tiles
     pack = make_pack([2000, 513, 257, 1], 3, 128, seed=70)
     dev = dev_inputs(pack)
     plain = {k: v.clone() for k, v in run_hip(pack, dev).items()}
@@ -53,9 +54,10 @@ def test_trace_records_and_results():
     assert 1 < len(cus) <= ncu and np.all((r[:, 0] >> np.uint64(16)) < 16)
 
 
-def test_trace_overflow_runs_untraced():
+def test_trace_overflow_runs_untraced(monkeypatch):
     import torch
-    pack = make_pack([700, 40], 2, 64, seed=71)  # keys > 512: wide (256-row) forward tiles
+    monkeypatch.setenv("T2V_QTILE", "wide")  # 256-row forward tiles
+    pack = make_pack([300, 40], 2, 64, seed=71)
     dev = dev_inputs(pack)
     nf = n_items(pack, 256)
     rec = torch.zeros(4 * nf, dtype=torch.int64, device="cuda")
