@@ -1,8 +1,8 @@
 // gfx950 kernels for packed variable-length bidirectional attention.
 //
 // One workgroup processes one work item (a tile of one clip and one head, from the host
-// scheduler): 8 waves / 256 queries in the forward and dQ kernels, 4 waves / 128 keys in
-// the dK/dV kernel. All products use v_mfma_f32_32x32x16_bf16 with fp32 accumulation;
+// scheduler): 8 waves / 256 queries (or 4 waves / 128 queries for short key segments) in
+// the forward and dQ kernels, 4 waves / 128 keys in the dK/dV kernel. All products use v_mfma_f32_32x32x16_bf16 with fp32 accumulation;
 // K/V (forward, dQ) or Q/dO (dK/dV) tiles are staged through LDS ahead of use (two
 // buffers in the forward and dQ kernels, four in dK/dV), one barrier per tile.
 //
@@ -16,10 +16,11 @@
 // exact for any reference m, so the result is the plain softmax up to rounding.
 //
 // Backward (Fig. 1 caption: the DiT backward pass): Delta = rowsum(dO * O), then a
-// dK/dV kernel (a workgroup owns 128 keys, loops over the clip's queries) and a dQ
-// kernel (a workgroup owns a query tile, loops over the clip's keys). P is recomputed
-// from the stored lse; nothing is accumulated across workgroups, so there are no
-// atomics and results are bitwise reproducible.
+// dK/dV kernel (a workgroup owns 128 keys, loops over the clip's queries, or over one
+// piece of them when the host splits long loops) and a dQ kernel (a workgroup owns a
+// query tile, loops over the clip's keys). P is recomputed from the stored lse; split
+// loops leave fp32 partial sums that a reduce kernel adds in a fixed order, so there are
+// no atomics and results are bitwise reproducible.
 #include "t2v_kernel_common.hpp"
 
 namespace t2v {
