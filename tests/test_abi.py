@@ -221,3 +221,50 @@ def test_trace_set_validation():
     assert "aligned" in _lib.t2v_last_error(L)
     assert L.t2v_trace_set(None, 0) == _lib.T2V_OK
     assert _lib.t2v_trace_count() == (0, 0)
+
+
+C_CONSUMER = r"""
+#include <stdio.h>
+#include "t2vattn.h"
+
+int main(void) {
+  const int32_t cu[4] = {0, 300, 300, 700};  /* the middle clip is empty */
+  int32_t items[4 * 16];
+  int n = -1;
+  double ms = 0.0, lb = 0.0;
+  if (t2v_build_worklist(cu, 3, 2, 256, T2V_ORDER_LONGEST_FIRST, NULL, 0, &n) != T2V_OK || n != 8) return 1;
+  if (t2v_build_worklist(cu, 3, 2, 256, T2V_ORDER_LONGEST_FIRST, items, 16, &n) != T2V_OK) return 2;
+  if (t2v_plan_makespan(items, n, 256, 4, &ms, &lb) != T2V_OK || ms < lb || lb <= 0.0) return 3;
+#ifdef WITH_GPU_LIBRARY
+  /* validation happens before any device work: a NULL tensor is refused */
+  if (t2v_attn_fwd(NULL, NULL, NULL, cu, 3, 2, 128, 0.1f, NULL, NULL, NULL) != T2V_ERR_INVALID_ARG) return 4;
+#else
+  if (t2v_build_worklist(NULL, 3, 2, 256, T2V_ORDER_LONGEST_FIRST, NULL, 0, &n) != T2V_ERR_INVALID_ARG) return 4;
+#endif
+  printf("%s | %s\n", t2v_version(), t2v_last_error());
+  return 0;
+}
+"""
+
+
+@pytest.mark.parametrize("lib", ["t2vattn_host", "t2vattn"])
+def test_header_is_plain_c_and_links(tmp_path, lib):
+    """A C99 program that includes only the public header, built with -pedantic -Werror,
+    links against the host-only and the GPU library and runs (no device work)."""
+    import shutil
+    import subprocess
+    if shutil.which("gcc") is None:
+        pytest.skip("gcc not available")
+    src = tmp_path / "consumer.c"
+    src.write_text(C_CONSUMER)
+    exe = str(tmp_path / "consumer")
+    libdir = os.path.dirname(_lib.LIB_PATH)
+    gpu = ["-DWITH_GPU_LIBRARY"] if lib == "t2vattn" else []
+    r = subprocess.run(["gcc", "-std=c99", "-Wall", "-Wextra", "-pedantic", "-Werror", *gpu, "-I",
+                        os.path.join(ROOT, "include"), str(src), "-o", exe, f"-L{libdir}", f"-l{lib}",
+                        f"-Wl,-rpath,{libdir}"], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stderr
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, (r.returncode, r.stdout, r.stderr)
+    assert "libt2vattn" in r.stdout
+    assert ("NULL" if lib == "t2vattn" else "cu_seqlens") in r.stdout  # the refused call's message
