@@ -35,24 +35,59 @@ int order_from_env() {
 // Q loads and output stores overlap another's MFMA work; wide tiles stage each K/V tile
 // once per 256 queries. Measured on MI355X (uniform packs): at D = 64 narrow is faster at
 // every length (8-19% forward, 4-12% dQ); at D = 128 the forward crosses over near 1,536
-// keys and dQ near 8,192-16,384. The length compared is the work-weighted key length
-// sum(Lq Lk^2) / sum(Lq Lk), so a mixed pack goes by the clips that dominate its time.
-// T2V_QTILE=wide or narrow forces one (ablations and tests).
-constexpr double kNarrowFwdKeys = 1536.0;
-constexpr double kNarrowDqKeys = 8192.0;
-
-bool narrow_tiles(const int32_t* cu_q, const int32_t* cu_k, int nseq, int head_dim, double max_keys) {
-  const char* s = std::getenv("T2V_QTILE");
-  if (s != nullptr && std::strcmp(s, "wide") == 0) return false;
-  if (s != nullptr && std::strcmp(s, "narrow") == 0) return true;
-  if (head_dim == 64) return true;
-  double work = 0.0, weighted = 0.0;
-  for (int i = 0; i < nseq; ++i) {
-    const double lq = cu_q[i + 1] - cu_q[i], lk = cu_k[i + 1] - cu_k[i];
-    work += lq * lk;
-    weighted += lq * lk * lk;
+// keys and dQ near 8,192-16,384, beyond which narrow tiles cost about 4% (forward) and 1%
+// (dQ) more per unit of work. choose_tile_rows compares the work-weighted key length with
+// those crossovers and, above them, the list-scheduling makespans of both work lists with
+// that penalty: a pack of few tiles per CU (one GPU's share of a long clip under head
+// sharding) loses more to a part-empty last round of wide tiles. T2V_QTILE=wide or narrow
+// forces one (ablations and tests).
+struct TileRule {
+  int kind = 0;  // 0: dK/dV (one tile shape), 1: forward, 2: dQ
+  int wide = 0, narrow = 0;
+  bool narrow_always = false;
+  double max_loop = 0.0, penalty = 1.0;
+  int forced = 0;  // 0: chosen by the rule, 1: wide, 2: narrow
+  bool same(const TileRule& o) const {
+    return kind == o.kind && wide == o.wide && narrow == o.narrow && narrow_always == o.narrow_always &&
+           forced == o.forced;
   }
-  return work <= 0.0 || weighted <= max_keys * work;
+};
+
+int forced_tiles() {
+  const char* s = std::getenv("T2V_QTILE");
+  if (s != nullptr && std::strcmp(s, "wide") == 0) return 1;
+  if (s != nullptr && std::strcmp(s, "narrow") == 0) return 2;
+  return 0;
+}
+
+TileRule fwd_rule(int head_dim) {
+  TileRule r;
+  r.kind = 1;
+  r.wide = fwd_tile_rows(head_dim, false);
+  r.narrow = fwd_tile_rows(head_dim, true);
+  r.narrow_always = head_dim == 64;
+  r.max_loop = 1536.0;
+  r.penalty = 1.04;
+  r.forced = forced_tiles();
+  return r;
+}
+
+TileRule dq_rule(int head_dim) {
+  TileRule r;
+  r.kind = 2;
+  r.wide = dq_tile_rows(head_dim, false);
+  r.narrow = dq_tile_rows(head_dim, true);
+  r.narrow_always = head_dim == 64;
+  r.max_loop = 8192.0;
+  r.penalty = 1.01;
+  r.forced = forced_tiles();
+  return r;
+}
+
+TileRule dkdv_rule(int head_dim) {
+  TileRule r;
+  r.wide = r.narrow = dkdv_tile_rows(head_dim);
+  return r;
 }
 
 // T2V_SPLIT=off disables the dK/dV loop split (for ablations).
@@ -103,6 +138,7 @@ int check_host_pointer(const int32_t* cu) {
 // another thread meanwhile stays alive; the last reference frees it.
 struct Plan {
   std::vector<int32_t> cu, cu_loop;  // offsets of the owned and the looped-over segments
+  TileRule rule;                     // how block was chosen (part of the key)
   int heads = 0, block = 0, order = 0, device = 0, chunk = 0;
   Item* d_items = nullptr;  // n_items work items, then n_reduce split tiles (loop split)
   Item* h_items = nullptr;  // pinned source of the upload, kept for the entry's life
@@ -128,8 +164,9 @@ class PlanCache {
  public:
   // Returns the plan (creating and uploading it on `stream` if new) with the
   // upload ordered before any later work on `stream`.
-  // chunk > 0: the loop split of build_worklist, with the reduce list after the items.
-  int get(const int32_t* cu, const int32_t* cu_loop, int nseq, int heads, int block, int order, int chunk,
+  // The tile rows follow `rule` (chosen once, when the plan is built; plan->block). chunk > 0:
+  // the loop split of build_worklist, with the reduce list after the items.
+  int get(const int32_t* cu, const int32_t* cu_loop, int nseq, int heads, const TileRule& rule, int order, int chunk,
           hipStream_t stream, PlanRef* out) {
     int device = 0;
     hipError_t e = hipGetDevice(&device);
@@ -138,7 +175,7 @@ class PlanCache {
     std::lock_guard<std::mutex> lock(mu_);
     for (auto itr = plans_.begin(); itr != plans_.end(); ++itr) {
       Plan& p = **itr;
-      if (p.heads == heads && p.block == block && p.order == order && p.device == device && p.chunk == chunk &&
+      if (p.heads == heads && p.rule.same(rule) && p.order == order && p.device == device && p.chunk == chunk &&
           p.cu.size() == static_cast<size_t>(nseq + 1) &&
           std::memcmp(p.cu.data(), cu, sizeof(int32_t) * (nseq + 1)) == 0 &&
           std::memcmp(p.cu_loop.data(), cu_loop, sizeof(int32_t) * (nseq + 1)) == 0) {
@@ -152,6 +189,18 @@ class PlanCache {
     PlanRef p = std::make_shared<Plan>();
     p->cu.assign(cu, cu + nseq + 1);
     p->cu_loop.assign(cu_loop, cu_loop + nseq + 1);
+    int ncu = 0;
+    if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess) {
+      (void)hipGetLastError();
+      ncu = 0;
+    }
+    const int block = rule.wide == rule.narrow ? rule.wide
+                      : rule.forced == 1       ? rule.wide
+                      : rule.forced == 2       ? rule.narrow
+                                               : choose_tile_rows(cu, cu_loop, nseq, heads, rule.wide, rule.narrow,
+                                                                  rule.narrow_always, rule.max_loop, rule.penalty,
+                                                                  order, ncu);
+    p->rule = rule;
     p->heads = heads;
     p->block = block;
     p->order = order;
@@ -166,8 +215,6 @@ class PlanCache {
     }
     const size_t bytes = items.size() * sizeof(Item);
     if (log_enabled()) {
-      int ncu = 0;
-      (void)hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, device);
       double ms = 0.0, lb = 0.0;
       plan_makespan(items.data(), p->n_items, block, ncu > 0 ? ncu : 1, &ms, &lb);
       std::fprintf(stderr,
@@ -371,11 +418,10 @@ int attn_fwd_impl(const void* q, const void* k, const void* v, const int32_t* cu
     if (int st = check_host_pointer(cu_k)) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   PlanRef plan;
-  const int rows = fwd_tile_rows(head_dim, narrow_tiles(cu_q, cu_k, nseq, head_dim, kNarrowFwdKeys));
-  if (int st = cache().get(cu_q, cu_k, nseq, heads, rows, order_from_env(), 0, s, &plan)) return st;
+  if (int st = cache().get(cu_q, cu_k, nseq, heads, fwd_rule(head_dim), order_from_env(), 0, s, &plan)) return st;
   if (plan->n_items == 0) return T2V_OK;
   AttnArgs a{};
-  a.q_rows = rows;
+  a.q_rows = plan->block;
   a.q = q;
   a.k = k;
   a.v = v;
@@ -417,15 +463,14 @@ int attn_bwd_impl(const void* q, const void* k, const void* v, const void* out, 
   // pieces whose fp32 partial sums go to slots in dq's memory: dq is an output that the dQ
   // kernel, launched after the reduce, overwrites, so the slots are capped at its size.
   const int kv_rows = dkdv_tile_rows(head_dim);
-  const int q_rows = dq_tile_rows(head_dim, narrow_tiles(cu_q, cu_k, nseq, head_dim, kNarrowDqKeys));
   int chunk = 0;
   if (split_enabled())
     chunk = choose_loop_split(cu_k, cu_q, nseq, heads, kv_rows, cu_count(), qb / dkdv_partial_slot_bytes(head_dim))
                 .chunk;
-  if (int st = cache().get(cu_k, cu_q, nseq, heads, kv_rows, order, chunk, s, &pk)) return st;
-  if (int st = cache().get(cu_q, cu_k, nseq, heads, q_rows, order, 0, s, &pq)) return st;
+  if (int st = cache().get(cu_k, cu_q, nseq, heads, dkdv_rule(head_dim), order, chunk, s, &pk)) return st;
+  if (int st = cache().get(cu_q, cu_k, nseq, heads, dq_rule(head_dim), order, 0, s, &pq)) return st;
   AttnArgs a{};
-  a.q_rows = q_rows;
+  a.q_rows = pq->block;
   a.partial = static_cast<float*>(dq);
   a.q = q;
   a.k = k;

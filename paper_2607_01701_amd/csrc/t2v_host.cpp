@@ -183,6 +183,26 @@ LoopSplit choose_loop_split(const int32_t* cu, const int32_t* cul, int nseq, int
   return {};
 }
 
+int choose_tile_rows(const int32_t* cu, const int32_t* cul, int nseq, int heads, int wide, int narrow,
+                     bool narrow_always, double narrow_max_loop, double narrow_penalty, int order, int slots) {
+  if (narrow_always) return narrow;
+  double work = 0.0, weighted = 0.0;
+  for (int s = 0; s < nseq; ++s) {
+    const double L = cu[s + 1] - cu[s], LL = cul[s + 1] - cul[s];
+    if (L <= 0 || LL <= 0) continue;
+    work += L * LL;
+    weighted += L * LL * LL;
+  }
+  if (work <= 0.0 || weighted <= narrow_max_loop * work) return narrow;
+  if (slots < 1) return wide;
+  double ms_wide = 0.0, ms_narrow = 0.0, lb = 0.0;
+  const std::vector<Item> w = build_worklist(cu, cul, nseq, heads, wide, order);
+  plan_makespan(w.data(), static_cast<int>(w.size()), wide, slots, &ms_wide, &lb);
+  const std::vector<Item> n = build_worklist(cu, cul, nseq, heads, narrow, order);
+  plan_makespan(n.data(), static_cast<int>(n.size()), narrow, slots, &ms_narrow, &lb);
+  return ms_narrow * narrow_penalty < ms_wide ? narrow : wide;
+}
+
 std::vector<Item> build_reduce_list(const int32_t* cu, const int32_t* cul, int nseq, int heads, int block,
                                     int chunk) {
   std::vector<Item> out;
@@ -208,29 +228,39 @@ std::vector<Item> build_worklist(const int32_t* cu, const int32_t* cu_loop, int 
   // self-attention this is the longest clip first); ties keep pack order, so one
   // (sequence, head)'s tiles stay adjacent.
   std::stable_sort(groups.begin(), groups.end(), [](const Group& a, const Group& b) { return a.llen > b.llen; });
-  // Workgroup b runs on XCD b % 8, and each XCD starts its share in increasing b.
-  // Deal whole (clip, head) groups to the least-loaded XCD that still has room, so the
-  // concurrently running tiles on one XCD read the same K/V through that XCD's L2,
-  // while every XCD carries about the same cost. Groups that fit nowhere are split.
+  // Workgroup b runs on XCD b % 8, and each XCD starts its share in increasing b, so every
+  // XCD takes the same number of items. Deal whole (clip, head) groups to the least-loaded
+  // XCD that has room for them and stays within an even share of the total cost, so the
+  // concurrently running tiles on one XCD read the same K/V through that XCD's L2. A group
+  // that fits nowhere (too many items, or too costly: few heavy groups, e.g. one long clip
+  // at a few heads) is split, filling the least-loaded XCD up to its share first.
   std::vector<size_t> cap(kNumXcd);
   for (int x = 0; x < kNumXcd; ++x) cap[x] = n / kNumXcd + (static_cast<size_t>(x) < n % kNumXcd ? 1 : 0);
   std::vector<std::vector<Item>> q(kNumXcd);
   std::vector<double> load(kNumXcd, 0.0);
+  double total = 0.0;
+  for (const auto& g : groups) total += static_cast<double>(g.tiles) * block * g.llen;
+  const double share = total / kNumXcd * (1.0 + 1e-9);
   for (const auto& g : groups) {
+    const double item_cost = static_cast<double>(block) * g.llen;
     int t = 0;
     while (t < g.tiles) {
       const size_t want = static_cast<size_t>(g.tiles - t);
       int best = -1;
       for (int x = 0; x < kNumXcd; ++x)  // least-loaded XCD with room for the rest of the group
-        if (cap[x] - q[x].size() >= want && (best < 0 || load[x] < load[best])) best = x;
+        if (cap[x] - q[x].size() >= want && load[x] + static_cast<double>(want) * item_cost <= share &&
+            (best < 0 || load[x] < load[best]))
+          best = x;
       size_t take = want;
-      if (best < 0) {  // split: least-loaded XCD with any room
+      if (best < 0) {  // split: the least-loaded XCD with any room, up to its share
         for (int x = 0; x < kNumXcd; ++x)
           if (cap[x] > q[x].size() && (best < 0 || load[x] < load[best])) best = x;
-        take = std::min(want, cap[best] - q[best].size());
+        const double fit = std::floor((share - load[best]) / item_cost);
+        const size_t under = fit >= 1.0 ? static_cast<size_t>(std::min(fit, 1e15)) : 1;
+        take = std::min({want, cap[best] - q[best].size(), under});
       }
       append_tiles(q[best], g, t, t + static_cast<int>(take), block);
-      load[best] += static_cast<double>(take) * block * g.llen;
+      load[best] += static_cast<double>(take) * item_cost;
       t += static_cast<int>(take);
     }
   }

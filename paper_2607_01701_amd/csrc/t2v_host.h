@@ -79,6 +79,16 @@ constexpr int kMinChunk = 2048;  // smallest piece: keeps the partial traffic sm
 LoopSplit choose_loop_split(const int32_t* cu_own, const int32_t* cu_loop, int nseq, int heads, int block,
                             int parallel, int64_t max_slots);
 
+// Tile rows for a kernel that comes in a wide and a narrow form (the forward and dQ
+// kernels: 256 or 128 query rows). Narrow when narrow_always, or when the work-weighted loop
+// length sum(L L'^2) / sum(L L') is at most narrow_max_loop (owned length L, looped-over
+// length L'); otherwise narrow only when the list-scheduling makespan of the narrow work list
+// over `slots` workers, times narrow_penalty (the narrow kernel's measured cost per unit of
+// work relative to the wide one on long loops), is below the wide list's: few tiles per CU
+// leave the last round of wide tiles part-empty.
+int choose_tile_rows(const int32_t* cu_own, const int32_t* cu_loop, int nseq, int heads, int wide, int narrow,
+                     bool narrow_always, double narrow_max_loop, double narrow_penalty, int order, int slots);
+
 // One item per split tile of build_worklist(..., chunk): row0, len, tile0, head of the tile,
 // slot = its first partial slot, pieces = the number of consecutive slots to sum.
 std::vector<Item> build_reduce_list(const int32_t* cu_own, const int32_t* cu_loop, int nseq, int heads, int block,

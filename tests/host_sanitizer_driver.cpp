@@ -162,6 +162,26 @@ static void loop_split(std::mt19937& rng) {
   CHECK(chosen >= 20, "the random packs exercise the split");
 }
 
+// Tile choice: narrow when forced by head_dim or short loops; on long loops, narrow only
+// where the wide list leaves the last round part-empty.
+static void tile_choice() {
+  const std::vector<int32_t> short_cu = {0, 300, 600};
+  CHECK(t2v::choose_tile_rows(short_cu.data(), short_cu.data(), 2, 24, 256, 128, false, 1536.0, 1.04,
+                              T2V_ORDER_LONGEST_FIRST, 256) == 128, "short loops: narrow");
+  const std::vector<int32_t> one = {0, 75600};
+  CHECK(t2v::choose_tile_rows(one.data(), one.data(), 1, 24, 256, 128, true, 1536.0, 1.04,
+                              T2V_ORDER_LONGEST_FIRST, 256) == 128, "narrow_always");
+  CHECK(t2v::choose_tile_rows(one.data(), one.data(), 1, 24, 256, 128, false, 1536.0, 1.04,
+                              T2V_ORDER_LONGEST_FIRST, 256) == 256, "long clip, 24 heads: wide");
+  CHECK(t2v::choose_tile_rows(one.data(), one.data(), 1, 3, 256, 128, false, 1536.0, 1.04,
+                              T2V_ORDER_LONGEST_FIRST, 256) == 128, "long clip, 3 heads: narrow (888 wide tiles)");
+  CHECK(t2v::choose_tile_rows(one.data(), one.data(), 1, 3, 256, 128, false, 1536.0, 1.04,
+                              T2V_ORDER_LONGEST_FIRST, 0) == 256, "no slots known: wide");
+  const std::vector<int32_t> none = {0, 0};
+  CHECK(t2v::choose_tile_rows(none.data(), none.data(), 1, 3, 256, 128, false, 1536.0, 1.04,
+                              T2V_ORDER_LONGEST_FIRST, 256) == 128, "empty pack");
+}
+
 // Validation: each rejected input yields the error it should, never a crash.
 static void validation(std::mt19937& rng) {
   int64_t T = 0, Tk = 0;
@@ -252,6 +272,7 @@ int main() {
   std::mt19937 rng(20260);
   worklists(rng);
   loop_split(rng);
+  tile_choice();
   validation(rng);
   planner(rng);
   std::printf("host sanitizer driver: %d failed checks\n", g_failed);

@@ -87,6 +87,22 @@ def test_xcd_cost_balance(name):
     assert per.max() <= 1.10 * per.mean()
 
 
+@pytest.mark.parametrize("name,heads", [("skew", 5), ("hetero", 3), ("long", 3), ("uniform", 3)])
+def test_xcd_cost_balance_with_few_heavy_groups(name, heads):
+    """One GPU's share under head sharding (a workload at H / 8 heads): few (clip, head)
+    groups, each heavier than an even XCD share. Equal item counts per XCD must not pin whole
+    heavy groups to some XCDs (before groups were split by cost: max / mean 1.59 for the
+    skewed pack at 5 heads, 1.40 for the heterogeneous mix at 3)."""
+    p = make_workload(name, tensors=False)
+    for block in (256, 128):
+        items = t2v_build_worklist(p.cu_seqlens, heads, block, ORDER_LONGEST_FIRST)
+        per, _ = _xcd_costs(items, block)
+        assert per.max() <= 1.08 * per.mean(), (block, per / per.mean())
+        mk, lb = t2v_plan_makespan(items, block, 256)
+        if block == 128:
+            assert mk <= 1.15 * lb, (mk, lb)
+
+
 @pytest.mark.parametrize("name", WORKLOADS)
 def test_workload_item_counts(name):
     """Item counts of the workloads at 128-row tiles of the query offsets (hetero and cross at seed 0;
