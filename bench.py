@@ -81,6 +81,9 @@ def parse_args():
     ap.add_argument("--balance", action="store_true",
                     help="trace one fwd+bwd step per scheduler order and print each kernel's per-CU busy-time "
                          "CV and idle share (the library's workgroup trace)")
+    ap.add_argument("--shares", action="store_true",
+                    help="time fwd+bwd at one GPU's share of the long, skew and hetero workloads under k-way head "
+                         "sharding (H / k heads, k = 1, 2, 4, 8), with the library's tile choice and forced tiles")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain device copy of known size (for HBM counter scaling)")
     ap.add_argument("--ingest-rocpd", nargs=5, metavar=("KT_DB", "FETCH_DB", "WRITE_DB", "COPY_FETCH_DB",
@@ -536,6 +539,85 @@ def cost_model_sweep(steps: int = 4, warmup: int = 2):
     return "\n".join(lines)
 
 
+def shares_report(seed: int = 0):
+    """One GPU's share of a workload under k-way head sharding (Ulysses sequence parallelism,
+    Section II-C: an All-to-All turns token sharding into head sharding, so each GPU runs
+    attention over the full cu_seqlens at H / k heads). Times fwd+bwd of the library at each
+    share shape, with the tile rows it chooses and with forced wide / narrow tiles, and the
+    host scheduler's predicted makespan over its lower bound for the forward work list."""
+    import numpy as np
+    import torch
+
+    from paper_2607_01701_amd import _lib
+    from paper_2607_01701_amd.workload import workload_shape
+
+    lines = ["Command (repo root, on the GPU): python3 bench.py --shares",
+             f"Kernel source hash (bench.py kernel_source_hash): {kernel_source_hash()}", "",
+             "One GPU's share under k-way head sharding: the workload's clips (seed 0) at H / k heads, D = 128,",
+             "inputs N(0,1) in bf16 drawn on the GPU (torch generator, seed 1); the All-to-All itself is not run.",
+             "TFLOP/s at 14 H D sum(L^2) per GPU; auto = the library's own tile choice; wide / narrow = forced",
+             "256- / 128-query forward and dQ tiles (T2V_QTILE); LPT = host list-scheduling makespan / lower bound",
+             "of the forward work list at the tile rows auto chose.", "",
+             f"{'workload':9s} {'k':>2s} {'heads':>5s} {'auto ms':>9s} {'auto TF/s':>9s} {'fwd rows':>8s} {'fwd tiles':>9s} "
+             f"{'wide TF/s':>9s} {'narrow TF/s':>11s} {'LPT':>6s}"]
+    ncu = torch.cuda.get_device_properties(0).multi_processor_count
+
+    def step(cu, q, k, v, g, scale, reps):
+        for _ in range(2):
+            o, lse = _lib.attn_fwd(q, k, v, cu, scale)
+            _lib.attn_bwd(q, k, v, o, lse, g, cu, scale)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            o, lse = _lib.attn_fwd(q, k, v, cu, scale)
+            _lib.attn_bwd(q, k, v, o, lse, g, cu, scale)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    for name, ks in (("long", (1, 2, 4, 8)), ("skew", (1, 2, 4, 8)), ("hetero", (1, 2, 4, 8))):
+        _, lens, H, D = workload_shape(name, seed)
+        cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+        T = int(cu[-1])
+        ssq = float(np.sum(np.asarray(lens, dtype=np.float64) ** 2))
+        for kdeg in ks:
+            h = H // kdeg
+            gen = torch.Generator(device="cuda").manual_seed(1)
+            q, k, v, g = (torch.randn(T, h, D, device="cuda", generator=gen).bfloat16() for _ in range(4))
+            reps = 3 if name != "hetero" else 10
+            flops = 14.0 * h * D * ssq
+            res = {}
+            for mode in ("auto", "wide", "narrow"):
+                if mode == "auto":
+                    os.environ.pop("T2V_QTILE", None)
+                else:
+                    os.environ["T2V_QTILE"] = mode
+                res[mode] = step(cu, q, k, v, g, D ** -0.5, reps)
+            os.environ.pop("T2V_QTILE", None)
+            # The forward tile rows the library chose: one traced forward takes one record per item.
+            n_wide = _lib.t2v_build_worklist(cu, h, 256, _lib.ORDER_LONGEST_FIRST).shape[0]
+            n_narrow = _lib.t2v_build_worklist(cu, h, 128, _lib.ORDER_LONGEST_FIRST).shape[0]
+            rec = torch.zeros(4 * max(n_wide, n_narrow), dtype=torch.int64, device="cuda")
+            _lib.t2v_trace_set(rec.data_ptr(), max(n_wide, n_narrow))
+            try:
+                _lib.attn_fwd(q, k, v, cu, D ** -0.5)
+                torch.cuda.synchronize()
+                n_traced, _ = _lib.t2v_trace_count()
+            finally:
+                _lib.t2v_trace_set(None, 0)
+            rows = 256 if n_traced == n_wide else 128
+            items = _lib.t2v_build_worklist(cu, h, rows, _lib.ORDER_LONGEST_FIRST)
+            mk, lb = _lib.t2v_plan_makespan(items, rows, ncu)
+            lines.append(f"{name:9s} {kdeg:2d} {h:5d} {res['auto']:9.3f} {flops / res['auto'] * 1e-9:9.1f} "
+                         f"{rows:8d} {items.shape[0]:9d} {flops / res['wide'] * 1e-9:9.1f} "
+                         f"{flops / res['narrow'] * 1e-9:11.1f} {mk / lb:6.3f}")
+            print(lines[-1], file=sys.stderr, flush=True)
+            del q, k, v, g
+            torch.cuda.empty_cache()
+    return "\n".join(lines)
+
+
 def balance_report(workload: str = "hetero", seed: int = 0):
     """Per-CU balance of each attention kernel on one traced fwd+bwd step, for both scheduler
     orders: per-CU busy time (summed workgroup durations from the library's workgroup trace),
@@ -631,8 +713,8 @@ def plan_batch_report(n_gpus: int = 16, seed: int = 0):
 
     lengths = workload_shape("hetero", seed)[1]
     layers, H, D = 60, 24, 128
-    alpha2 = 4.542753e-08 * 1e-3 * layers        # s per token^2, attention fwd+bwd, all layers (fitted, 24 x 128)
-    alpha1_attn = 9.616564e-06 * 1e-3 * layers   # s per token (fitted)
+    alpha2 = 4.721237e-08 * 1e-3 * layers        # s per token^2, attention fwd+bwd, all layers (fitted, 24 x 128)
+    alpha1_attn = 1.051087e-05 * 1e-3 * layers   # s per token (fitted)
     alpha1_rest = 4 * 2 * 3 * (H * D) ** 2 * 12 / 1.0e15 * layers / (H * D)  # MLP+proj GEMMs at 1 PF/s, s/token
     hidden_bytes = H * D * 2
     a2a_bw = 7 * 153e9                           # xGMI: 7 links x ~153 GB/s per GPU
@@ -898,6 +980,9 @@ def main():
         return
     if args.balance:
         print(balance_report(args.workload, args.seed), flush=True)
+        return
+    if args.shares:
+        print(shares_report(args.seed), flush=True)
         return
     if args.sweep:
         # Smaller step counts for the long workloads keep the sweep to about a minute of GPU time.
