@@ -264,6 +264,35 @@ std::vector<Item> build_worklist(const int32_t* cu, const int32_t* cu_loop, int 
       t += static_cast<int>(take);
     }
   }
+  // With few groups the item-count capacity can still leave the XCDs' costs uneven. Then
+  // deal single items instead (longest first, each to the least-loaded XCD with room),
+  // which balances cost at the price of spreading each group's K/V over all XCDs' L2s
+  // (measured: 0.6% slower where group dealing balances, 3-5% faster where it does not).
+  auto imbalance = [](const std::vector<double>& l) {
+    double mx = 0.0, sum = 0.0;
+    for (double x : l) {
+      mx = std::max(mx, x);
+      sum += x;
+    }
+    return sum > 0.0 ? mx * static_cast<double>(l.size()) / sum : 1.0;
+  };
+  const double grouped = imbalance(load);
+  if (grouped > 1.01) {
+    std::vector<std::vector<Item>> qi(kNumXcd);
+    std::vector<double> li(kNumXcd, 0.0);
+    for (const auto& g : groups) {
+      std::vector<Item> tiles;
+      append_tiles(tiles, g, 0, g.tiles, block);
+      for (const Item& it : tiles) {
+        int best = -1;
+        for (int x = 0; x < kNumXcd; ++x)
+          if (cap[x] > qi[x].size() && (best < 0 || li[x] < li[best])) best = x;
+        qi[best].push_back(it);
+        li[best] += static_cast<double>(block) * it.llen;
+      }
+    }
+    if (imbalance(li) < grouped) q.swap(qi);
+  }
   items.resize(n);
   for (size_t b = 0; b < n; ++b) items[b] = q[b % kNumXcd][b / kNumXcd];
   return items;
