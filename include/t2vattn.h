@@ -34,7 +34,10 @@
  * Tiles. The forward and dQ kernels own 256-query tiles (8 waves, one workgroup per CU)
  * or 128-query tiles (4 waves, two or three per CU): narrow tiles at head_dim 64, and at
  * 128 when the work-weighted key length sum(Lq Lk^2) / sum(Lq Lk) is at most 1,536 (forward)
- * or 8,192 (dQ), where they were measured faster. Both give bitwise-equal results. The dK/dV kernel owns 128-key tiles and loops over the
+ * or 8,192 (dQ), where they were measured faster, or when the host's list-scheduling model
+ * predicts that the wide tiles would leave CUs idle in a part-empty last round (packs with
+ * few tiles per CU, e.g. a long clip at a few heads). The choice is made once per new work
+ * list. Both shapes give bitwise-equal results. The dK/dV kernel owns 128-key tiles and loops over the
  * sequence's queries; when the costliest such loop exceeds an even share of the work over
  * the GPU's CUs (few, short key segments against long query segments, as in
  * cross-attention to text), the loops are cut into pieces of at least 2048 queries whose
