@@ -54,6 +54,9 @@ SPLIT_PACKS = [
     # (name, query lengths, key lengths, heads, head_dim, expected piece rows)
     ("split_d128", [9000, 300, 4500, 0, 2600], [100, 50, 256, 0, 1], 2, 128, 2048),
     ("split_d64", [7000, 2100, 65], [33, 500, 129], 3, 64, 2048),
+    # dq holds 30,000 / 512 = 58 slots: pieces of 2,048 (120 slots) and 4,096 (64) do not
+    # fit, so the split widens to 8,192-query pieces (4 per tile, 32 slots)
+    ("split_widened", [30000], [1000], 1, 128, 8192),
 ]
 
 
