@@ -1,5 +1,8 @@
-// Backward dK/dV kernel: a workgroup owns 128 keys of one (clip, head) and loops over
-// the clip's queries (see t2v_fwd.hip for the shared design notes).
+// Backward dK/dV kernel: a workgroup owns 32 keys per wave of one (clip, head) and loops
+// over the clip's queries (see t2v_fwd.hip for the shared design notes). At head_dim 128
+// four waves (128 keys, one workgroup per CU: 502 VGPRs) stage 64-query tiles; at 64, eight
+// waves (256 keys, two per SIMD) share 128-query tiles, so each staged Q / dO tile feeds
+// twice the waves (measured: +1-1.5% per fwd+bwd step at D = 64, results bitwise equal).
 #include "t2v_kernel_common.hpp"
 
 namespace t2v {
@@ -10,7 +13,14 @@ namespace {
 
 constexpr int kDkdvBM = 64;     // queries per LDS stage (a multiple of 32)
 constexpr int kDkdvStages = 4;  // LDS stages: up to 3 tiles of Q / dO in flight during one tile's work
-constexpr int kDkdvKeys = (kThreads / 64) * 32;  // keys per workgroup: 32 per wave
+// Threads, queries per LDS stage and keys per workgroup by head_dim (32 keys per wave; each
+// wave stages one 32-float piece of lse2 or -Delta per stage, so 2 BM = 32 waves).
+template <int D>
+constexpr int dkdv_threads() { return D == 64 ? 512 : kThreads; }
+template <int D>
+constexpr int dkdv_bm() { return D == 64 ? 128 : kDkdvBM; }
+template <int D>
+constexpr int dkdv_keys() { return dkdv_threads<D>() / 64 * 32; }
 
 // Asynchronous copy of consecutive floats into LDS, one per active lane of the calling
 // wave: lane i copies row i0 + off + i, clamped to L - 1, to lds[i]. The tile's first row
@@ -124,7 +134,7 @@ T2V_DEV void dkdv_step(uint32_t qbase, uint32_t gbase, uint32_t qr0, uint32_t qr
 }
 
 template <int D>
-__global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
+__global__ __launch_bounds__(dkdv_threads<D>(), 1) void attn_bwd_dkdv_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
     const bf16* __restrict__ dout, const float* __restrict__ lse2, const float* __restrict__ ndelta,
     const Item* __restrict__ items, int H, int64_t T, float c, float scale, bf16* __restrict__ dk,
@@ -132,9 +142,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
   const unsigned long long trace_t0 = trace != nullptr ? trace_clock() : 0ull;
   constexpr int KK = D / 16;
   constexpr int DB = D / 32;
-  constexpr int BM = kDkdvBM;      // queries per LDS stage
+  constexpr int BM = dkdv_bm<D>();  // queries per LDS stage
   constexpr int NS = kDkdvStages;  // LDS stages in flight
-  constexpr int NW = kThreads / 64;
+  constexpr int NW = dkdv_threads<D>() / 64;
   // DMA instructions per wave and stage: the Q and dO tiles, plus one 32-float piece of
   // lse * log2(e) or -Delta.
   constexpr int kOps = 2 * (BM * D / 512) / NW + 1;
@@ -164,7 +174,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
   const bool wave_active = key_wave0 < Lk;
 
   // Every wave issues exactly kOps DMA instructions per stage, so counted waits work.
-  const TileDma<D, BM, kThreads> dma(tid, rs);
+  const TileDma<D, BM, dkdv_threads<D>()> dma(tid, rs);
   auto stage = [&](int t) {
     const int b = t % NS, i0 = t * BM;
     dma.copy(sQ[b], qh, rs, i0, L);
@@ -251,8 +261,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_bwd_dkdv_kernel(
   if (wave_active && it.slot >= 0) {
     // One piece of a split loop: unscaled fp32 sums into the item's partial slot
     // ([dK | dV] x tile key x head dim), added up in piece order by the reduce kernel.
-    float* pk = partial + static_cast<int64_t>(it.slot) * (2 * kDkdvKeys * D);
-    float* pv = pk + kDkdvKeys * D;
+    float* pk = partial + static_cast<int64_t>(it.slot) * (2 * dkdv_keys<D>() * D);
+    float* pv = pk + dkdv_keys<D>() * D;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int kr = wave * 32 + (r >> 2) * 8 + G * 4 + (r & 3);  // key within the tile
@@ -287,19 +297,19 @@ template <int D>
 __global__ __launch_bounds__(kThreads) void dkdv_reduce_kernel(const float* __restrict__ partial,
                                                                const Item* __restrict__ tiles, int H, float scale,
                                                                bf16* __restrict__ dk, bf16* __restrict__ dv) {
-  constexpr int kQuarters = kDkdvKeys / 32;
+  constexpr int kQuarters = dkdv_keys<D>() / 32;
   constexpr int C4 = D / 4;  // float4 columns per key row
   const Item it = tiles[blockIdx.x / kQuarters];
   const int k0 = (blockIdx.x % kQuarters) * 32;  // first key of this block, within the tile
   const int nkeys = min(32, it.len - it.tile0 - k0);
   const int64_t rs = static_cast<int64_t>(H) * D;
-  const int64_t slot_elems = 2 * kDkdvKeys * D;
+  const int64_t slot_elems = 2 * dkdv_keys<D>() * D;
   for (int e = threadIdx.x; e < 2 * 32 * C4; e += kThreads) {
     const int which = e / (32 * C4);  // 0: dK, 1: dV
     const int r = (e / C4) % 32;
     const int c4 = e % C4;
     if (r >= nkeys) continue;
-    const float* src = partial + static_cast<int64_t>(it.slot) * slot_elems + which * kDkdvKeys * D +
+    const float* src = partial + static_cast<int64_t>(it.slot) * slot_elems + which * dkdv_keys<D>() * D +
                        (k0 + r) * D + c4 * 4;
     f32x4 acc = *reinterpret_cast<const f32x4*>(src);
     for (int p = 1; p < it.pieces; ++p) {
@@ -321,12 +331,12 @@ __global__ __launch_bounds__(kThreads) void dkdv_reduce_kernel(const float* __re
 
 }  // namespace
 
-int dkdv_tile_rows(int) { return kDkdvKeys; }
+int dkdv_tile_rows(int head_dim) { return head_dim == 64 ? dkdv_keys<64>() : dkdv_keys<128>(); }
 
-int64_t dkdv_partial_slot_bytes(int head_dim) { return 2LL * kDkdvKeys * head_dim * 4; }
+int64_t dkdv_partial_slot_bytes(int head_dim) { return 2LL * dkdv_tile_rows(head_dim) * head_dim * 4; }
 
 hipError_t launch_bwd_dkdv_reduce(const AttnArgs& a, const Item* tiles, int n_tiles, hipStream_t stream) {
-  const dim3 grid(n_tiles * (kDkdvKeys / 32)), block(kThreads);
+  const dim3 grid(n_tiles * (dkdv_tile_rows(a.head_dim) / 32)), block(kThreads);
   auto* dk = static_cast<bf16*>(a.dk);
   auto* dv = static_cast<bf16*>(a.dv);
   if (a.head_dim == 128)
@@ -338,7 +348,7 @@ hipError_t launch_bwd_dkdv_reduce(const AttnArgs& a, const Item* tiles, int n_ti
 
 hipError_t launch_bwd_dkdv(const AttnArgs& a, const Item* items, int n_items, hipStream_t stream) {
   const float c = a.scale * kLog2e;
-  const dim3 grid(n_items), block(kThreads);
+  const dim3 grid(n_items), block(a.head_dim == 64 ? dkdv_threads<64>() : dkdv_threads<128>());
   const auto* q = static_cast<const bf16*>(a.q);
   const auto* k = static_cast<const bf16*>(a.k);
   const auto* v = static_cast<const bf16*>(a.v);
