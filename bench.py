@@ -713,8 +713,8 @@ def plan_batch_report(n_gpus: int = 16, seed: int = 0):
 
     lengths = workload_shape("hetero", seed)[1]
     layers, H, D = 60, 24, 128
-    alpha2 = 4.511540e-08 * 1e-3 * layers        # s per token^2, attention fwd+bwd, all layers (fitted, 24 x 128)
-    alpha1_attn = 9.652105e-06 * 1e-3 * layers   # s per token (fitted)
+    alpha2 = 4.634277e-08 * 1e-3 * layers        # s per token^2, attention fwd+bwd, all layers (fitted, 24 x 128)
+    alpha1_attn = 1.351341e-05 * 1e-3 * layers   # s per token (fitted)
     alpha1_rest = 4 * 2 * 3 * (H * D) ** 2 * 12 / 1.0e15 * layers / (H * D)  # MLP+proj GEMMs at 1 PF/s, s/token
     hidden_bytes = H * D * 2
     a2a_bw = 7 * 153e9                           # xGMI: 7 links x ~153 GB/s per GPU
