@@ -144,6 +144,98 @@ def test_oracle_mutants_are_caught(name):
     assert failing, f"mutant {name} passed every pin"
 
 
+# ---------------------------------------------------------------- checker pins
+#
+# The checker decides whether a schedule satisfies Eqs. (2)-(7); the planner's validity claims
+# rest on it. Each negative case below breaks exactly one constraint of a schedule the checker
+# must accept, so a checker that skips that constraint (or accepts everything) fails a pin.
+# Instance: 0 -> 2 (precedence), three cascades, K = {1, 3}, N = 3, W = 1.
+CHK = dict(preds=[[], [], [0]], degrees=[1, 3], latency=[[2.0, 1.5], [3.0, 2.0], [1.0, 0.75]],
+           mem=[[0.5, 0.25], [2.0, 0.9], [0.5, 0.25]], mem_cap=1.0, n_gpus=3)
+# Valid: 0 at k = 1 on [0, 2), 1 at k = 3 on [2, 4) (it does not fit one GPU: Mem = 2 > W),
+# 2 at k = 1 on [4, 5): makespan 5. Touching intervals (an end equal to a start) are legal.
+CHK_VALID = ([1, 3, 1], [0.0, 2.0, 4.0], 5.0)
+CHK_BAD = {
+    # Eq. (4): cascade 2 runs on [1, 2), before its predecessor 0 ends at 2 (two GPUs busy).
+    "precedence": ([1, 3, 1], [0.0, 2.0, 1.0], "predecessor"),
+    # Eq. (5): degree 2 is not in K = {1, 3}, although two GPUs are free for it.
+    "degree_not_in_K": ([1, 3, 2], [0.0, 2.0, 4.0], "not in K"),
+    # Eq. (6): cascade 1 at k = 1 needs Mem = 2 > W = 1; it runs alone on [2, 5).
+    "memory": ([1, 1, 1], [0.0, 2.0, 5.0], "memory"),
+    # Eq. (7): 0 (k = 1) on [0, 2) and 1 (k = 3) on [1, 3) overlap: four GPUs in use > N = 3.
+    "capacity": ([1, 3, 1], [0.0, 1.0, 3.0], "GPUs in use"),
+    # Eq. (7) with usage rising at a start inside an interval that began earlier: 1 (k = 3) on
+    # [0, 2), then 0 (k = 1) from 1.5; 2 after 0.
+    "capacity_late_start": ([1, 3, 1], [1.5, 0.0, 3.5], "GPUs in use"),
+}
+
+
+def test_checker_accepts_the_valid_schedule():
+    deg, st, T = CHK_VALID
+    ok, T2, msg = milp.check_schedule(CHK["preds"], CHK["degrees"], CHK["latency"], CHK["mem"], CHK["mem_cap"],
+                                      CHK["n_gpus"], deg, st)
+    assert ok, msg
+    assert T2 == T
+
+
+@pytest.mark.parametrize("name", sorted(CHK_BAD))
+def test_checker_rejects_one_broken_constraint(name):
+    deg, st, why = CHK_BAD[name]
+    ok, _, msg = milp.check_schedule(CHK["preds"], CHK["degrees"], CHK["latency"], CHK["mem"], CHK["mem_cap"],
+                                     CHK["n_gpus"], deg, st)
+    assert not ok and why in msg, (name, msg)
+
+
+def test_checker_pins_are_one_constraint_each():
+    """Each negative case differs from a legal schedule by one constraint only: with that one
+    constraint relaxed (N = 3 for capacity, W = 2 for memory, K widened, the edge dropped) the
+    same schedule is accepted."""
+    relax = {"precedence": dict(preds=[[], [], []]), "degree_not_in_K": dict(degrees=[1, 3, 2]),
+             "memory": dict(mem_cap=2.0), "capacity": dict(n_gpus=4), "capacity_late_start": dict(n_gpus=4)}
+    for name, (deg, st, _) in CHK_BAD.items():
+        args = dict(CHK)
+        args.update(relax[name])
+        lat, mem = args["latency"], args["mem"]
+        if len(args["degrees"]) == 3:  # K widened: latency / memory columns for k = 3
+            lat = [row + [row[-1]] for row in lat]
+            mem = [row + [row[-1]] for row in mem]
+        ok, _, msg = milp.check_schedule(args["preds"], args["degrees"], lat, mem, args["mem_cap"], args["n_gpus"],
+                                         deg, st)
+        assert ok, (name, msg)
+
+
+def _checker_pins_hold(mod):
+    args = (CHK["preds"], CHK["degrees"], CHK["latency"], CHK["mem"], CHK["mem_cap"], CHK["n_gpus"])
+    deg, st, T = CHK_VALID
+    ok, T2, _ = mod.check_schedule(*args, deg, st)
+    if not ok or T2 != T:
+        return False
+    return all(not mod.check_schedule(*args, d, s)[0] for d, s, _ in CHK_BAD.values())
+
+
+CHECKER_MUTANTS = {
+    "accept_everything": ("    n = len(preds)\n    if len(deg) != n", "    return True, 0.0, 'ok'\n    n = len(preds)\n    if len(deg) != n"),
+    "no_precedence": ("            if starts[c] < end[p] - tol:", "            if False:"),
+    # an unknown degree read as the largest one in K
+    "no_degree_set": ("        if deg[c] not in degrees:\n            return False, None, f\"cascade {c}: degree {deg[c]} not in K\"  # Eq. (5)\n        j = degrees.index(deg[c])",
+                      "        j = degrees.index(deg[c]) if deg[c] in degrees else len(degrees) - 1"),
+    "no_memory": ("        if mem[c][j] > mem_cap:", "        if False:"),
+    "no_capacity": ("        if used > n_gpus:", "        if False:"),
+    "capacity_at_time_zero_only": ("    for t in sorted(set(starts)):", "    for t in [0.0]:"),
+    "end_is_latency": ("    end = [starts[c] + lat[c] for c in range(n)]", "    end = [lat[c] for c in range(n)]"),
+}
+
+
+def test_checker_pins_hold_for_the_checker():
+    assert _checker_pins_hold(milp)
+
+
+@pytest.mark.parametrize("name", sorted(CHECKER_MUTANTS))
+def test_checker_mutants_are_caught(name):
+    mod = _mutant(*CHECKER_MUTANTS[name])
+    assert not _checker_pins_hold(mod), f"checker mutant {name} passed every pin"
+
+
 # ---------------------------------------------------------------- native planner
 
 def test_library_exports_planner():
