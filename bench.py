@@ -64,6 +64,8 @@ def parse_args():
     ap.add_argument("--workload", default="hetero", help="tiny | uniform | hetero | long | skew")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="headline workload only: skip the per-workload summary and the fresh-pack comparison")
     ap.add_argument("--write-summaries", nargs="+", metavar=("BENCH_JSON", "SWEEP_JSONL"),
                     help="write the text summaries under profiles/ from a bench line, profiles/hbm_traffic.json "
                          "and (optionally) a --sweep output")
@@ -93,6 +95,22 @@ def parse_args():
     ap.add_argument("--ingest-mfma", metavar="PMC_DB",
                     help="summarise a rocprofv3 MfmaUtil / MfmaFlopsBF16 counter pass into profiles/; runs on the CPU")
     return ap.parse_args()
+
+
+# The paper's own numbers are end-to-end training iteration times on another machine; quoted
+# as context only (they measure no attention kernel and are not comparable to this metric).
+PAPER_CONTEXT = {
+    "hardware": "NVIDIA H100-80GB, 8 GPUs per node (NVLink), 8 x 400 Gbps InfiniBand; PyTorch 2.7.1, CUDA 12.6; "
+                "16 GPUs end to end, up to 64 for scalability",
+    "avg_iteration_time_s": {"HunyuanVideo-13B stage 1 (360p)": 22.07, "stage 2 (720p)": 32.96,
+                             "stage 3 (1080p)": 26.80},
+    "iteration_time_reduction_vs": {"Megatron-LM": "up to 65%", "DeepSpeed": "up to 59%", "FlexSP": "up to 35%"},
+    "case_study_step_s": {"static DP=4 x SP=4 slowest rank": 58.6, "fastest rank": 6.0, "FlexSP": 45.2,
+                          "Arachne": 31.4},
+    "note": "Section V-B (end-to-end), V-D (ablation table) and V-E / Section III (case study: static, FlexSP "
+            "and Arachne schedules of one step); no attention-kernel time or throughput is published, so "
+            "vs_baseline is null",
+}
 
 
 def kernel_flops(H, D, ssq):
@@ -425,6 +443,65 @@ def write_summaries(bench_json, sweep_jsonl=None):
 
 # Model shapes of the paper's Table II (hidden size / heads = head_dim): 1536/12, 3072/24, 1920/30.
 COST_SHAPES = ((12, 128), (24, 128), (30, 64))
+# Table II: model, layers, heads, head_dim (hidden = heads x head_dim).
+TABLE2_MODELS = (("Wan2.1-1.3B", 30, 12, 128), ("CogVideoX-5B", 30, 30, 64), ("HunyuanVideo-13B", 60, 24, 128))
+GEMM_TOKENS = (4096, 16384, 65536)
+DIT_COST_FILE = os.path.join(ROOT, "profiles", "dit_cost_model.json")
+
+
+def gemm_proxy_sweep(steps: int = 5, warmup: int = 2):
+    """alpha_1 of Eq. (9), measured: the linear operations of one DiT block, forward and
+    backward, as bf16 GEMMs on the GPU (torch.matmul, i.e. the vendor BLAS; a measurement
+    outside libt2vattn). Per token of hidden size d: the QKV projection (d x 3d), the attention
+    output projection (d x d) and the MLP (d x 4d, 4d x d), each forward (X W), and backward
+    (dX = dY W^T, dW = X^T dY): 72 d^2 flops per token. Fits t_ms = alpha1 * tokens + c per
+    Table II hidden size over GEMM_TOKENS tokens. Returns {hidden: (alpha1_ms_per_token, c_ms,
+    TFLOP/s at the largest size, rows)}."""
+    import numpy as np
+    import torch
+
+    out = {}
+    for name, layers, H, D in TABLE2_MODELS:
+        d = H * D
+        gen = torch.Generator(device="cuda").manual_seed(d)
+        shapes = [(d, 3 * d), (d, d), (d, 4 * d), (4 * d, d)]
+        W = [torch.randn(a, b, generator=gen, device="cuda").to(torch.bfloat16) / a ** 0.5 for a, b in shapes]
+        rows = []
+        for n in GEMM_TOKENS:
+            X = [torch.randn(n, a, generator=gen, device="cuda").to(torch.bfloat16) for a, _ in shapes]
+            dY = [torch.randn(n, b, generator=gen, device="cuda").to(torch.bfloat16) for _, b in shapes]
+            Wt = [w.t().contiguous() for w in W]
+            Xt = [x.t().contiguous() for x in X]  # every operand contiguous (no transposed views)
+
+            def block():
+                for x, xt, w, wt, dy in zip(X, Xt, W, Wt, dY):
+                    torch.matmul(x, w)            # forward
+                    torch.matmul(dy, wt)          # dX
+                    torch.matmul(xt, dy)          # dW
+
+            for _ in range(warmup):
+                block()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(steps):
+                block()
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / steps
+            rows.append((n, ms))
+            print(f"[cost-model] GEMM proxy d={d} tokens={n}: {ms:.3f} ms "
+                  f"({72.0 * d * d * n / (ms * 1e-3) * 1e-12:.0f} TFLOP/s)", file=sys.stderr, flush=True)
+            del X, Xt, dY, Wt
+        A = np.array([[n, 1.0] for n, _ in rows])
+        t = np.array([ms for _, ms in rows])
+        w = 1.0 / t
+        coef, *_ = np.linalg.lstsq(A * w[:, None], t * w, rcond=None)
+        n_big, ms_big = rows[-1]
+        out[d] = (float(coef[0]), float(coef[1]), 72.0 * d * d * n_big / (ms_big * 1e-3) * 1e-12, rows)
+        del W
+        torch.cuda.empty_cache()
+    return out
 COST_SEQ = (1024, 2048, 4096, 8192, 16384, 32768)
 COST_BATCH = (1, 2, 4, 8)
 COST_MAX_TOKENS = 65536
@@ -536,6 +613,39 @@ def cost_model_sweep(steps: int = 4, warmup: int = 2):
     av = np.asarray(all_val)
     lines.append(f"All shapes, held-out packs: rms relative error {100 * float(np.sqrt(np.mean(av ** 2))):.2f}%, "
                  f"max {100 * float(np.max(np.abs(av))):.2f}%")
+    # alpha_1: the block's linear operations, measured as GEMMs (not part of libt2vattn).
+    gem = gemm_proxy_sweep()
+    lines.append("")
+    lines.append("alpha_1 of Eq. (9), measured: the linear operations of one DiT block (QKV d x 3d, output d x d, MLP "
+                 "d x 4d and 4d x d), forward and backward (72 d^2 flops per token), as bf16 torch.matmul GEMMs:")
+    lines.append("  hidden d   tokens   ms      TFLOP/s   -> alpha1_linear (ms/token)   c (ms)")
+    models = {}
+    for name, layers, H, D in TABLE2_MODELS:
+        d = H * D
+        a1, c1, tf, rows = gem[d]
+        for n, ms in rows:
+            lines.append(f"  {d:8d} {n:8d} {ms:8.3f} {72.0 * d * d * n / (ms * 1e-3) * 1e-12:9.0f}")
+        lines.append(f"  {d:8d}  fit: alpha1_linear = {a1:.6e} ms/token, c = {c1:.4f} ms")
+        fs = [x for x in fit_samples if x[1] == H and x[2] == D]
+        model, _ = costmodel.fit(fs)
+        models[name] = {"layers": layers, "heads": H, "head_dim": D, "hidden": d,
+                        "alpha2_ms_per_token2": model.alpha2(H, D), "alpha1_attention_ms_per_token": model.alpha1(H, D),
+                        "c0_attention_ms": model.c0, "alpha1_linear_ms_per_token": a1, "c_linear_ms": c1,
+                        "gemm_tflops_at_65536_tokens": round(tf, 1)}
+    lines.append("")
+    lines.append("L_{c,k=1} per Table II model (one DiT cascade, fwd + bwd of all layers; k = 1, no communication):")
+    lines.append("  L(B, S) = layers * ((alpha1_linear + alpha1_attention) * B*S + alpha2 * B*S^2)")
+    for name, m in models.items():
+        a1 = m["layers"] * (m["alpha1_linear_ms_per_token"] + m["alpha1_attention_ms_per_token"])
+        a2 = m["layers"] * m["alpha2_ms_per_token2"]
+        lines.append(f"  {name:17s} ({m['layers']} layers, {m['heads']} x {m['head_dim']}): alpha1 = {a1:.4e} ms/token, "
+                     f"alpha2 = {a2:.4e} ms/token^2; e.g. one 20,280-token clip: {a1 * 20280 + a2 * 20280 ** 2:.0f} ms, "
+                     f"attention share {100 * a2 * 20280 ** 2 / (a1 * 20280 + a2 * 20280 ** 2):.0f}%")
+    with open(DIT_COST_FILE, "w") as f:
+        json.dump({"kernel_source_hash": kernel_source_hash(), "models": models,
+                   "note": "alpha2 and alpha1_attention: libt2vattn fwd+bwd per layer (fitted); alpha1_linear: the "
+                           "block's GEMMs fwd+bwd per layer (torch.matmul, measured); written by bench.py --cost-model"},
+                  f, indent=1, sort_keys=True)
     return "\n".join(lines)
 
 
@@ -699,12 +809,12 @@ def plan_batch_report(n_gpus: int = 16, seed: int = 0):
 
     Each clip of the heterogeneous mix is three cascades: VAE encode -> DiT forward/backward,
     and a text encoder -> the same DiT cascade. The DiT's latency at degree k follows Eq. (9):
-    (alpha_1 S + alpha_2 S^2) / k for the attention of 60 layers (HunyuanVideo-13B shape, 24 x 128,
-    coefficients of the MI355X attention cost model in profiles/attn_cost_model_sweep.txt), a
-    linear per-token term of the same size standing in for the rest of the block, and an
-    All-to-All term for k > 1 over xGMI; memory follows Eq. (8). The VAE and text-encoder
-    latencies are linear in tokens. Every constant not measured here is stated below and is
-    an assumption of this synthetic batch, not a measurement.
+    (alpha_1 S + alpha_2 S^2) / k over 60 layers (HunyuanVideo-13B shape, 24 x 128), with alpha_2
+    and the attention's per-token term fitted to libt2vattn and alpha_1 of the block's linear
+    operations measured as bf16 GEMMs (both by --cost-model on the GPU), plus an All-to-All
+    term for k > 1 over xGMI; memory follows Eq. (8). The VAE and text-encoder latencies are
+    linear in tokens. Every constant not measured is stated below and is an assumption of
+    this synthetic batch, not a measurement.
     """
     import numpy as np
 
@@ -712,10 +822,15 @@ def plan_batch_report(n_gpus: int = 16, seed: int = 0):
     from paper_2607_01701_amd.workload import workload_shape
 
     lengths = workload_shape("hetero", seed)[1]
-    layers, H, D = 60, 24, 128
-    alpha2 = 4.634277e-08 * 1e-3 * layers        # s per token^2, attention fwd+bwd, all layers (fitted, 24 x 128)
-    alpha1_attn = 1.351341e-05 * 1e-3 * layers   # s per token (fitted)
-    alpha1_rest = 4 * 2 * 3 * (H * D) ** 2 * 12 / 1.0e15 * layers / (H * D)  # MLP+proj GEMMs at 1 PF/s, s/token
+    # Measured coefficients (bench.py --cost-model on the GPU, profiles/dit_cost_model.json):
+    # attention alpha_2 and its per-token term from libt2vattn, alpha_1 of the block's linear
+    # operations from the GEMM proxy; per layer, fwd + bwd, in ms.
+    with open(DIT_COST_FILE) as f:
+        m = json.load(f)["models"]["HunyuanVideo-13B"]
+    layers, H, D = m["layers"], m["heads"], m["head_dim"]
+    alpha2 = m["alpha2_ms_per_token2"] * 1e-3 * layers                # s per token^2, all layers
+    alpha1_attn = m["alpha1_attention_ms_per_token"] * 1e-3 * layers  # s per token
+    alpha1_rest = m["alpha1_linear_ms_per_token"] * 1e-3 * layers      # s per token: the block's GEMMs
     hidden_bytes = H * D * 2
     a2a_bw = 7 * 153e9                           # xGMI: 7 links x ~153 GB/s per GPU
     W = 288e9                                    # bytes per GPU
@@ -747,10 +862,11 @@ def plan_batch_report(n_gpus: int = 16, seed: int = 0):
     lines = ["Command (repo root, CPU only): python3 bench.py --plan", "",
              f"Cascade plan of one batch: the heterogeneous mix (seed {seed}, {len(lengths)} clips) as {n} cascades "
              f"on N = {n_gpus} GPUs, degrees K = {K} (Section IV-A, Eqs. (1)-(7); Alg. 1).",
-             "Latency inputs: DiT attention from the MI355X cost model (24 x 128, 60 layers: alpha2 = "
-             f"{alpha2:.3e} s/token^2, alpha1 = {alpha1_attn:.3e} s/token); assumed: rest of the block "
-             f"{alpha1_rest:.3e} s/token, All-to-All over 7 x 153 GB/s xGMI, VAE 2e-6 s/token / k^0.9, "
-             "text encoder 0.02 s / k^0.5; memory Eq. (8) with assumed constants, W = 288 GB.",
+             "Latency inputs, measured on one MI355X (profiles/dit_cost_model.json, HunyuanVideo-13B shape: "
+             f"{layers} layers, {H} x {D}): attention alpha2 = {alpha2:.3e} s/token^2 and {alpha1_attn:.3e} s/token "
+             f"(libt2vattn), the block's linear operations alpha1 = {alpha1_rest:.3e} s/token (bf16 GEMM proxy); "
+             "assumed: All-to-All over 7 x 153 GB/s xGMI, VAE 2e-6 s/token / k^0.9, text encoder 0.02 s / k^0.5; "
+             "memory Eq. (8) with assumed constants, W = 288 GB.",
              f"GA: population 64, 300 generations, planning time {t_plan:.2f} s (host CPU, one thread).",
              f"Planned makespan: {T:.2f} s", "", "Static parallel degree for every cascade (list-scheduled, same DAG):"]
     for k in K:
@@ -788,9 +904,19 @@ def mfma_probe(blocks: int = 2048, iters: int = 40000) -> dict:
                       f"{blocks} workgroups x {iters} rounds"}
 
 
-def run_workload(workload, seed, steps, warmup, order=None):
+def device_normal(shape, gen):
+    """bf16 N(0,1) values drawn on the GPU from a seeded generator (timing-only inputs)."""
+    import torch
+    return torch.randn(shape, generator=gen, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+
+
+def run_workload(workload, seed, steps, warmup, order=None, device_values=False):
     """Times `steps` fwd+bwd steps of one workload after `warmup` untimed ones; returns the
-    bench record (without the CPU baseline) and the pack."""
+    bench record (without the CPU baseline) and the pack.
+
+    device_values: draw the N(0,1) inputs on the GPU (seeded) instead of on the host; the
+    timing-only summaries of the other workloads use this, since drawing the largest packs
+    on the host takes longer than timing them."""
     import numpy as np
     import torch
 
@@ -800,7 +926,7 @@ def run_workload(workload, seed, steps, warmup, order=None):
     if order is not None:
         os.environ["T2V_ORDER"] = order  # read by the library at each call
     t_gen = time.perf_counter()
-    pack = make_workload(workload, seed=seed)
+    pack = make_workload(workload, seed=seed, tensors=not device_values)
     H, D, T = pack.heads, pack.head_dim, pack.total_tokens
     print(f"[bench] workload {workload}: T={T} H={H} D={D} sum(Lq*Lk)={pack.sum_qk} "
           f"(generated in {time.perf_counter() - t_gen:.1f}s)", file=sys.stderr, flush=True)
@@ -808,7 +934,12 @@ def run_workload(workload, seed, steps, warmup, order=None):
     def dev(bits):
         return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
 
-    q, k, v, g = dev(pack.q), dev(pack.k), dev(pack.v), dev(pack.dout)
+    if device_values:
+        gen = torch.Generator(device="cuda").manual_seed(seed)
+        Tk = pack.total_tokens_k if pack.cu_seqlens_k is not None else T
+        q, k, v, g = (device_normal((n, H, D), gen) for n in (T, Tk, Tk, T))
+    else:
+        q, k, v, g = dev(pack.q), dev(pack.k), dev(pack.v), dev(pack.dout)
     out = torch.empty_like(q)
     dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(k)
     lse = torch.empty((H, T), dtype=torch.float32, device="cuda")
@@ -947,6 +1078,120 @@ def run_workload(workload, seed, steps, warmup, order=None):
     return res, pack
 
 
+# The default line's summary of every workload: (name, timed steps, warmup steps). The long
+# and skewed packs take 0.26 and 0.77 s per step, so they get few.
+WORKLOAD_STEPS = (("tiny", 50, 10), ("uniform", 20, 5), ("long", 4, 1), ("skew", 3, 1))
+
+
+def workloads_summary(seed: int, main_res: dict) -> dict:
+    """fwd and fwd+bwd TFLOP/s, fraction of the bf16 peak and ms per step of the five workloads
+    (the heterogeneous mix from the headline run, the others timed here with inputs drawn on
+    the GPU)."""
+    out = {}
+
+    def entry(r, steps):
+        return {"fwd_bwd_tflops": r["value"], "frac_of_peak": r["frac_of_peak"], "fwd_tflops": r["fwd_tflops"],
+                "fwd_frac_of_peak": round(r["fwd_tflops"] / PEAK_BF16_TFLOPS, 4), "ms_per_step": r["ms_per_step"],
+                "fwd_ms": r["timing"]["fwd"]["median_ms"], "steps": steps,
+                "config": r["config"]["workload"], "sum_sq_len": r["config"]["sum_sq_len"]}
+
+    for name, steps, warmup in WORKLOAD_STEPS[:2]:
+        r, _ = run_workload(name, seed, steps, warmup, device_values=True)
+        out[name] = entry(r, steps)
+    out["hetero"] = entry(main_res, main_res["steps"])
+    for name, steps, warmup in WORKLOAD_STEPS[2:]:
+        r, _ = run_workload(name, seed, steps, warmup, device_values=True)
+        out[name] = entry(r, steps)
+    return out
+
+
+def fresh_pack_report(seed: int = 0, n_base: int = 16, steps: int = 32) -> dict:
+    """Cost of a new cu_seqlens on every call (clip lengths change from batch to batch,
+    Section III, Observation 1) against the cached-plan path, on the same GPU work.
+
+    Base packs: the heterogeneous mix at seeds seed .. seed + n_base - 1. Cached: the steps
+    cycle over the base packs, whose work lists (3 per pack, 48 in all) stay in the library's
+    cache. Fresh: each step takes the next base pack with its clips in a new random order, a
+    cu_seqlens the library has not seen, so every call builds, uploads and caches new work
+    lists and, past 64 lists, releases old ones. Both runs do the same clips per step, so
+    the difference is the cache-miss cost as the GPU sees it."""
+    import numpy as np
+    import torch
+
+    from paper_2607_01701_amd import _lib
+    from paper_2607_01701_amd.workload import cu_from_lengths, workload_shape
+
+    base = [list(workload_shape("hetero", seed + i)[1]) for i in range(n_base)]
+    _, _, H, D = workload_shape("hetero", seed)
+    tmax = max(sum(b) for b in base)
+    gen = torch.Generator(device="cuda").manual_seed(seed + 7)
+    q, k, v, g = (device_normal((tmax, H, D), gen) for _ in range(4))
+    out, dq, dk, dv = (torch.empty_like(q) for _ in range(4))
+    lse = torch.empty((H, tmax), dtype=torch.float32, device="cuda")
+    ws = torch.empty((2, H, tmax), dtype=torch.float32, device="cuda")
+    L = _lib.lib()
+    stream = torch.cuda.current_stream()
+    sh = stream.cuda_stream
+    sc = 1.0 / D ** 0.5
+    rng = np.random.default_rng(seed + 11)
+    seen = set()
+
+    def step(lengths):
+        cu = np.ascontiguousarray(cu_from_lengths(lengths), dtype=np.int32)
+        cup = cu.ctypes.data_as(_lib._i32p)
+        st = L.t2v_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), cup, len(lengths), H, D, sc, out.data_ptr(),
+                            lse.data_ptr(), sh)
+        if st == 0:
+            st = L.t2v_attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(), cup,
+                                len(lengths), H, D, sc, g.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
+                                ws.data_ptr(), sh)
+        if st:
+            raise _lib.T2VError(st, _lib.t2v_last_error())
+
+    def fresh(i):
+        while True:
+            b = base[i % n_base]
+            perm = [b[j] for j in rng.permutation(len(b))]
+            if tuple(perm) not in seen and perm != b:
+                seen.add(tuple(perm))
+                return perm
+
+    def timed(lengths_of):
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        h0 = time.perf_counter()
+        e0.record(stream)
+        for i in range(steps):
+            step(lengths_of(i))
+        e1.record(stream)
+        host_ms = (time.perf_counter() - h0) * 1e3 / steps
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps, host_ms
+
+    _lib.t2v_release_cache()
+    for b in base:  # cached: every base pack's three work lists built once
+        step(b)
+    for i in range(3):
+        step(fresh(i))
+    cached_ms, cached_host = timed(lambda i: base[i % n_base])
+    fresh_ms, fresh_host = timed(lambda i: fresh(i))
+    ssq = sum(sum(x * x for x in base[i % n_base]) for i in range(steps)) / steps
+    fl = 14.0 * H * D * ssq
+    del q, k, v, g, out, dq, dk, dv, lse, ws
+    torch.cuda.empty_cache()
+    res = {"cached_ms_per_step": round(cached_ms, 4), "fresh_ms_per_step": round(fresh_ms, 4),
+           "cached_tflops": round(fl / (cached_ms * 1e-3) * 1e-12, 2),
+           "fresh_tflops": round(fl / (fresh_ms * 1e-3) * 1e-12, 2),
+           "overhead_pct": round(100.0 * (fresh_ms / cached_ms - 1.0), 2),
+           "host_ms_per_call_pair": {"cached": round(cached_host, 3), "fresh": round(fresh_host, 3)},
+           "steps": steps,
+           "packs": f"hetero mix, seeds {seed}..{seed + n_base - 1}; fresh steps permute a base pack's clip order "
+                    f"(new cu_seqlens every call: 3 new work lists per fwd+bwd, 64 cached)"}
+    print(f"[bench] fresh packs: cached {cached_ms:.3f} ms/step, fresh {fresh_ms:.3f} ms/step "
+          f"({res['overhead_pct']:+.2f}%)", file=sys.stderr, flush=True)
+    return res
+
+
 def main():
     args = parse_args()
     if args.ingest_rocpd:
@@ -996,6 +1241,10 @@ def main():
     res, pack = run_workload(args.workload, args.seed, args.steps, args.warmup)
     res["mfma_probe"] = mfma_probe()
     res["roofline"]["frac_of_probe"] = round(res["roofline"]["achieved"] / res["mfma_probe"]["tflops"], 4)
+    if args.workload == "hetero" and not args.no_extras:
+        res["workloads"] = workloads_summary(args.seed, res)
+        res["fresh_packs"] = fresh_pack_report(args.seed)
+        res["paper_context"] = PAPER_CONTEXT
     if not args.no_cpu_baseline:
         print("[bench] timing the float64 oracle on a bounded sample", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(pack)

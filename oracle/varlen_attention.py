@@ -236,11 +236,12 @@ def key_rows(q, k, v, dout, cu_seqlens, scale: float, seq: int, head: int, keys,
 
 
 def key_rows_torch(q, k, v, dout, cu_seqlens, scale: float, seq: int, head: int, keys,
-                   block_rows: int = 2048, cu_seqlens_k=None) -> dict:
+                   block_rows: int = 2048, cu_seqlens_k=None, progress=None) -> dict:
     """``key_rows`` with torch float64 CPU tensor operations (multithreaded matmul and exp).
 
     Same steps as ``key_rows``; used for the 75,600- and 100,800-token clips, where one
-    head's full score matrix is about 10^10 entries.
+    head's full score matrix is about 10^10 entries. ``progress(r1, L)``, if given, is
+    called after each block of query rows (long runs report how far they are).
     """
     import torch
     cu = np.asarray(cu_seqlens, dtype=np.int64)
@@ -270,4 +271,6 @@ def key_rows_torch(q, k, v, dout, cu_seqlens, scale: float, seq: int, head: int,
         dSc = Pc * (dOb @ Vs.T - db[:, None])
         dv += Pc.T @ dOb
         dk += scale * (dSc.T @ Qb)
+        if progress is not None:
+            progress(r1, L)
     return {"dk": dk.numpy(), "dv": dv.numpy()}

@@ -234,10 +234,35 @@ def _stream_handle(stream):
     return s.cuda_stream
 
 
-def _check_tensor(t, name, T, H, D):
+def _check_tensor(t, name, shape, dtype=None):
+    """Shape, dtype, layout and device of a tensor passed to the library, checked in that order
+    (the library sees only pointers, so a wrong size would be read or written past its end)."""
     import torch
-    if not t.is_cuda or t.dtype != torch.bfloat16 or not t.is_contiguous() or tuple(t.shape) != (T, H, D):
-        raise ValueError(f"{name} must be a contiguous CUDA bfloat16 tensor of shape {(T, H, D)}")
+    dtype = torch.bfloat16 if dtype is None else dtype
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _check_on_device(named):
+    """Last of the checks: every tensor is on a GPU (the same one as the first)."""
+    first = None
+    for name, t in named:
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be a CUDA tensor")
+        if first is None:
+            first = t.device
+        elif t.device != first:
+            raise ValueError(f"{name} is on {t.device}, the other tensors on {first}")
+
+
+def _check_offsets(cu: np.ndarray, rows: int, name: str):
+    """The last offset must equal the packed tensor's row count (T = cu_seqlens[nseq])."""
+    if int(cu[-1]) != int(rows):
+        raise ValueError(f"{name}[-1] = {int(cu[-1])} does not match the {int(rows)} rows of the packed tensors")
 
 
 def attn_fwd(q, k, v, cu_seqlens, scale: float, out=None, lse=None, stream=None, cu_seqlens_k=None):
@@ -249,14 +274,20 @@ def attn_fwd(q, k, v, cu_seqlens, scale: float, out=None, lse=None, stream=None,
     import torch
     T, H, D = q.shape
     Tk = T if cu_seqlens_k is None else k.shape[0]
-    _check_tensor(q, "q", T, H, D)
+    _check_tensor(q, "q", (T, H, D))
     for name, t in (("k", k), ("v", v)):
-        _check_tensor(t, name, Tk, H, D)
+        _check_tensor(t, name, (Tk, H, D))
     cu = _cu_array(cu_seqlens)
+    _check_offsets(cu, T, "cu_seqlens")
+    if cu_seqlens_k is not None:
+        _check_offsets(_cu_array(cu_seqlens_k), Tk, "cu_seqlens_k")
     if out is None:
         out = torch.empty_like(q)
     if lse is None:
         lse = torch.empty((H, T), dtype=torch.float32, device=q.device)
+    _check_tensor(out, "out", (T, H, D))
+    _check_tensor(lse, "lse", (H, T), torch.float32)
+    _check_on_device((("q", q), ("k", k), ("v", v), ("out", out), ("lse", lse)))
     L = lib()
     if cu_seqlens_k is None:
         st = L.t2v_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), cu.ctypes.data_as(_i32p), cu.shape[0] - 1, H,
@@ -277,15 +308,25 @@ def attn_bwd(q, k, v, out, lse, dout, cu_seqlens, scale: float, dq=None, dk=None
     T, H, D = q.shape
     Tk = T if cu_seqlens_k is None else k.shape[0]
     for name, t in (("q", q), ("out", out), ("dout", dout)):
-        _check_tensor(t, name, T, H, D)
+        _check_tensor(t, name, (T, H, D))
     for name, t in (("k", k), ("v", v)):
-        _check_tensor(t, name, Tk, H, D)
+        _check_tensor(t, name, (Tk, H, D))
+    _check_tensor(lse, "lse", (H, T), torch.float32)
     cu = _cu_array(cu_seqlens)
+    _check_offsets(cu, T, "cu_seqlens")
+    if cu_seqlens_k is not None:
+        _check_offsets(_cu_array(cu_seqlens_k), Tk, "cu_seqlens_k")
     dq = torch.empty_like(q) if dq is None else dq
     dk = torch.empty_like(k) if dk is None else dk
     dv = torch.empty_like(k) if dv is None else dv
     if delta_ws is None:
         delta_ws = torch.empty((2, H, T), dtype=torch.float32, device=q.device)
+    _check_tensor(dq, "dq", (T, H, D))
+    _check_tensor(dk, "dk", (Tk, H, D))
+    _check_tensor(dv, "dv", (Tk, H, D))
+    _check_tensor(delta_ws, "delta_ws", (2, H, T), torch.float32)
+    _check_on_device((("q", q), ("k", k), ("v", v), ("out", out), ("lse", lse), ("dout", dout), ("dq", dq),
+                      ("dk", dk), ("dv", dv), ("delta_ws", delta_ws)))
     L = lib()
     if cu_seqlens_k is None:
         st = L.t2v_attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),

@@ -10,6 +10,7 @@ from __future__ import annotations
 
 import concurrent.futures as cf
 import os
+import re
 import shutil
 import subprocess
 import sys
@@ -44,13 +45,58 @@ SCHED = {
 }
 
 
-def _run(cmd, verbose):
+# Every kernel is compiled with the compiler's per-kernel resource report, and the build
+# fails if any kernel spills registers or uses scratch (private) memory. The kernels order
+# their LDS DMA with counted `s_waitcnt vmcnt(N)` waits that assume only the DMA
+# instructions are outstanding; spill stores and reloads are vector memory operations too,
+# and would silently shift those counts (a wait would then return before its stage landed).
+RESOURCE_REMARKS = ["-Rpass-analysis=kernel-resource-usage"]
+_REMARK = re.compile(r"remark:\s+(Function Name|ScratchSize \[bytes/lane\]|SGPRs Spill|VGPRs Spill|"
+                     r"Dynamic Stack|VGPRs|AGPRs):\s+(\S+)")
+
+
+def kernel_resources(compiler_output: str) -> dict:
+    """{kernel: {field: value}} from the compiler's kernel-resource-usage remarks."""
+    res, cur = {}, None
+    for line in compiler_output.splitlines():
+        m = _REMARK.search(line)
+        if not m:
+            continue
+        key, val = m.group(1), m.group(2)
+        if key == "Function Name":
+            cur = res.setdefault(val, {})
+        elif cur is not None:
+            cur[key] = val
+    return res
+
+
+def resource_violations(resources: dict) -> list:
+    """Kernels that spill or use scratch memory (each as a readable line)."""
+    bad = []
+    for name, r in sorted(resources.items()):
+        why = [f"{k} = {r[k]}" for k in ("ScratchSize [bytes/lane]", "SGPRs Spill", "VGPRs Spill")
+               if r.get(k, "0") != "0"]
+        if r.get("Dynamic Stack", "False") != "False":
+            why.append("dynamic stack")
+        if why:
+            bad.append(f"{name}: {', '.join(why)}")
+    return bad
+
+
+def _run(cmd, verbose, check_resources=False):
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
-    out = "\n".join(line for line in r.stdout.splitlines() if "packed-fp32-ops" not in line)
+    lines = [line for line in r.stdout.splitlines() if "packed-fp32-ops" not in line]
+    out = "\n".join(line for line in lines if "kernel-resource-usage" not in line)
     if r.returncode != 0:
         raise RuntimeError(f"command failed ({r.returncode}): {' '.join(cmd)}\n{out}")
+    if check_resources:
+        res = kernel_resources(r.stdout)
+        bad = resource_violations(res)
+        if bad:
+            raise RuntimeError("kernels spill registers or use scratch memory (not allowed: the counted LDS-DMA "
+                               "waits assume no other vector memory traffic):\n  " + "\n  ".join(bad))
     if verbose and out.strip():
         print(out, flush=True)
 
@@ -62,13 +108,14 @@ def build(verbose: bool = True) -> None:
     for s in HIP_SOURCES:
         o = os.path.join(BUILD, s + ".o")
         objs.append(o)
-        jobs.append([HIPCC, *HIP_FLAGS, *SCHED.get(s, []), "-c", os.path.join(CSRC, s), "-o", o])
+        jobs.append(([HIPCC, *HIP_FLAGS, *SCHED.get(s, []), *RESOURCE_REMARKS, "-c", os.path.join(CSRC, s), "-o", o],
+                     True))
     for s in HOST_SOURCES:
         o = os.path.join(BUILD, s + ".o")
         objs.append(o)
-        jobs.append([CXX, *COMMON, "-c", os.path.join(CSRC, s), "-o", o])
+        jobs.append(([CXX, *COMMON, "-c", os.path.join(CSRC, s), "-o", o], False))
     with cf.ThreadPoolExecutor(max_workers=6) as ex:
-        for f in [ex.submit(_run, j, verbose) for j in jobs]:
+        for f in [ex.submit(_run, j, verbose, chk) for j, chk in jobs]:
             f.result()
     tmp = LIB + ".tmp"
     _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp], verbose)

@@ -133,30 +133,228 @@ int check_host_pointer(const int32_t* cu) {
   return T2V_OK;
 }
 
+// Both offset arrays are read on the host (validation, scheduling), so they are checked to
+// be host memory before anything dereferences them, including the T = 0 early return.
+int check_offsets_on_host(const int32_t* cu_q, const int32_t* cu_k) {
+  if (cu_q == nullptr) return set_error(T2V_ERR_INVALID_ARG, "cu_seqlens is NULL");
+  if (int st = check_host_pointer(cu_q)) return st;
+  if (cu_k != cu_q) {
+    if (cu_k == nullptr) return set_error(T2V_ERR_INVALID_ARG, "cu_seqlens_k is NULL");
+    if (int st = check_host_pointer(cu_k)) return st;
+  }
+  return T2V_OK;
+}
+
+// Memory for work lists, per device: device chunks hold the lists the kernels read, pinned
+// host chunks stage their uploads. Lists are carved out of the chunks by RangeAllocator, so a
+// new list costs no hipMalloc / hipHostMalloc once the chunks are large enough (a chunk is
+// added, at twice the size of the last, only when none has room). A range is handed back
+// only after every event recorded behind its readers has completed: the upload's event for
+// a staging range, and the last launch on each stream that read a device range. Nothing
+// here waits for the device.
+class ListPool {
+ public:
+  struct Block {
+    int chunk = -1;
+    uint64_t off = 0, bytes = 0;
+    void* ptr = nullptr;
+  };
+  explicit ListPool(bool pinned) : pinned_(pinned) {}
+
+  // Caller holds mu(). Returns T2V_OK and a block of `bytes`, or T2V_ERR_OOM.
+  int alloc(uint64_t bytes, Block* out) {
+    if (fail_alloc_for_test()) return set_error(T2V_ERR_OOM, "allocation of work-list memory failed (forced)");
+    if (try_alloc(bytes, out)) return T2V_OK;
+    reclaim();
+    if (try_alloc(bytes, out)) return T2V_OK;
+    uint64_t size = last_size_ == 0 ? (pinned_ ? kFirstPinned : kFirstDevice) : 2 * last_size_;
+    while (size < RangeAllocator::rounded(bytes)) size *= 2;
+    void* base = nullptr;
+    const hipError_t e = pinned_ ? hipHostMalloc(&base, size, hipHostMallocDefault) : hipMalloc(&base, size);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return set_error(T2V_ERR_OOM, pinned_ ? "hipHostMalloc of work-list staging failed"
+                                            : "hipMalloc of work-list memory failed");
+    }
+    chunks_.push_back({base, RangeAllocator(size)});
+    last_size_ = size;
+    return try_alloc(bytes, out) ? T2V_OK : set_error(T2V_ERR_OOM, "work-list pool");
+  }
+
+  // Caller holds mu(). The block returns to its chunk once `events` (taken over) complete.
+  void release_after(const Block& b, std::vector<hipEvent_t> events) {
+    if (b.chunk < 0) {
+      recycle_events(events);
+      return;
+    }
+    pending_.push_back({b, std::move(events)});
+  }
+
+  // Caller holds mu(). An event from the pool (or a new one), for recording.
+  hipError_t take_event(hipEvent_t* ev) {
+    if (!events_.empty()) {
+      *ev = events_.back();
+      events_.pop_back();
+      return hipSuccess;
+    }
+    return hipEventCreateWithFlags(ev, hipEventDisableTiming);
+  }
+  void recycle_events(std::vector<hipEvent_t>& evs) {
+    for (hipEvent_t e : evs) events_.push_back(e);
+    evs.clear();
+  }
+
+  // Caller holds the lock and has synchronised the device: returns every pending block and
+  // frees each chunk that no live block uses (a list still held by a call in progress keeps
+  // its chunk), and the idle events.
+  void trim_after_sync() {
+    reclaim();
+    for (auto& c : chunks_) {
+      if (c.base == nullptr || c.alloc.free_bytes() != c.alloc.size()) continue;
+      if (pinned_)
+        (void)hipHostFree(c.base);
+      else
+        (void)hipFree(c.base);
+      c.base = nullptr;
+      c.alloc = RangeAllocator(0);  // an empty slot: indices of live blocks stay valid
+    }
+    for (hipEvent_t e : events_) (void)hipEventDestroy(e);
+    events_.clear();
+  }
+
+ private:
+  static constexpr uint64_t kFirstDevice = 4u << 20, kFirstPinned = 2u << 20;
+  struct Chunk {
+    void* base;
+    RangeAllocator alloc;
+  };
+  struct Pending {
+    Block block;
+    std::vector<hipEvent_t> events;
+  };
+  bool try_alloc(uint64_t bytes, Block* out) {
+    for (int c = static_cast<int>(chunks_.size()) - 1; c >= 0; --c) {  // newest (largest) chunk first
+      const int64_t off = chunks_[c].alloc.alloc(bytes);
+      if (off < 0) continue;
+      *out = {c, static_cast<uint64_t>(off), bytes, static_cast<char*>(chunks_[c].base) + off};
+      return true;
+    }
+    return false;
+  }
+  // Returns every pending block whose events have all completed.
+  void reclaim() {
+    for (auto it = pending_.begin(); it != pending_.end();) {
+      bool done = true;
+      for (hipEvent_t e : it->events) {
+        if (hipEventQuery(e) != hipSuccess) {  // not reached yet (or the query failed: keep the block)
+          (void)hipGetLastError();
+          done = false;
+          break;
+        }
+      }
+      if (!done) {
+        ++it;
+        continue;
+      }
+      (void)chunks_[it->block.chunk].alloc.release(it->block.off, it->block.bytes);
+      recycle_events(it->events);
+      it = pending_.erase(it);
+    }
+  }
+  bool pinned_;
+  uint64_t last_size_ = 0;  // size of the newest chunk: the next one doubles it
+  std::vector<Chunk> chunks_;
+  std::list<Pending> pending_;
+  std::vector<hipEvent_t> events_;
+};
+
+// Both pools of one device, and the lock that guards them.
+struct DevicePools {
+  std::mutex mu;
+  ListPool dev{false}, pin{true};
+};
+
+std::mutex& pools_mu() {
+  static std::mutex* mu = new std::mutex();
+  return *mu;
+}
+std::vector<DevicePools*>& all_pools() {
+  static std::vector<DevicePools*>* all = new std::vector<DevicePools*>();  // never destroyed
+  return *all;
+}
+
+DevicePools& pools(int device) {
+  std::lock_guard<std::mutex> lock(pools_mu());
+  auto& all = all_pools();
+  if (device >= static_cast<int>(all.size())) all.resize(device + 1, nullptr);
+  if (all[device] == nullptr) all[device] = new DevicePools();
+  return *all[device];
+}
+
+// After a device-wide synchronisation: gives back the memory of every list no longer held.
+void trim_pools_after_sync() {
+  std::vector<DevicePools*> all;
+  {
+    std::lock_guard<std::mutex> lock(pools_mu());
+    all = all_pools();
+  }
+  for (DevicePools* p : all) {
+    if (p == nullptr) continue;
+    std::lock_guard<std::mutex> lock(p->mu);
+    p->dev.trim_after_sync();
+    p->pin.trim_after_sync();
+  }
+}
+
 // Immutable device copies of work lists, keyed by everything that shapes them. Calls hold
-// a shared reference from lookup until their launches are enqueued, so an entry evicted by
-// another thread meanwhile stays alive; the last reference frees it.
+// a shared reference from lookup until their launches are enqueued and the launches' event
+// is recorded (note_use), so an entry evicted by another thread meanwhile stays alive; when
+// the last reference goes, its device block returns to the pool after those events.
 struct Plan {
   std::vector<int32_t> cu, cu_loop;  // offsets of the owned and the looped-over segments
   TileRule rule;                     // how block was chosen (part of the key)
   int heads = 0, block = 0, order = 0, device = 0, chunk = 0;
   Item* d_items = nullptr;  // n_items work items, then n_reduce split tiles (loop split)
-  Item* h_items = nullptr;  // pinned source of the upload, kept for the entry's life
   int n_items = 0, n_reduce = 0;
-  hipEvent_t ready = nullptr;  // upload finished
+  ListPool::Block mem;             // d_items' block in the device pool
+  hipEvent_t ready = nullptr;      // upload finished (from the device pool's event pool)
+  std::vector<std::pair<hipStream_t, hipEvent_t>> uses;  // last launch reading d_items, per stream
   ~Plan() {
-    // Launches on any stream may still read d_items: let the plan's device finish first.
-    int cur = -1;
-    const bool other = hipGetDevice(&cur) == hipSuccess && cur != device;
-    if (other) (void)hipSetDevice(device);
-    (void)hipDeviceSynchronize();
-    if (d_items != nullptr) (void)hipFree(d_items);
-    if (h_items != nullptr) (void)hipHostFree(h_items);
-    if (ready != nullptr) (void)hipEventDestroy(ready);
-    if (other) (void)hipSetDevice(cur);
+    DevicePools& p = pools(device);
+    std::lock_guard<std::mutex> lock(p.mu);
+    std::vector<hipEvent_t> evs;
+    if (ready != nullptr) evs.push_back(ready);
+    for (auto& u : uses) evs.push_back(u.second);
+    p.dev.release_after(mem, std::move(evs));
   }
 };
 using PlanRef = std::shared_ptr<Plan>;
+
+// Records, on `stream`, the point after which the launches just enqueued no longer read the
+// plan's list. Later launches on the same stream replace the earlier event (stream order).
+int note_use(const PlanRef& plan, hipStream_t stream) {
+  DevicePools& p = pools(plan->device);
+  std::lock_guard<std::mutex> lock(p.mu);
+  hipEvent_t ev = nullptr;
+  hipError_t e = p.dev.take_event(&ev);
+  if (e == hipSuccess) e = hipEventRecord(ev, stream);
+  if (e != hipSuccess) {
+    if (ev != nullptr) (void)hipEventDestroy(ev);
+    // Without the event the list could be reused under a running kernel: keep it alive.
+    (void)hipStreamSynchronize(stream);
+    return hip_fail(e, "hipEventRecord after launch");
+  }
+  for (auto& u : plan->uses) {
+    if (u.first == stream) {
+      std::vector<hipEvent_t> old{u.second};
+      p.dev.recycle_events(old);
+      u.second = ev;
+      return T2V_OK;
+    }
+  }
+  plan->uses.push_back({stream, ev});
+  return T2V_OK;
+}
 
 constexpr size_t kMaxPlans = 64;
 
@@ -180,8 +378,10 @@ class PlanCache {
           std::memcmp(p.cu.data(), cu, sizeof(int32_t) * (nseq + 1)) == 0 &&
           std::memcmp(p.cu_loop.data(), cu_loop, sizeof(int32_t) * (nseq + 1)) == 0) {
         plans_.splice(plans_.begin(), plans_, itr);  // most recently used first
-        e = hipStreamWaitEvent(stream, p.ready, 0);
-        if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
+        if (p.ready != nullptr) {
+          e = hipStreamWaitEvent(stream, p.ready, 0);
+          if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
+        }
         *out = *itr;
         return T2V_OK;
       }
@@ -194,19 +394,20 @@ class PlanCache {
       (void)hipGetLastError();
       ncu = 0;
     }
+    std::vector<Item> items;
     const int block = rule.wide == rule.narrow ? rule.wide
                       : rule.forced == 1       ? rule.wide
                       : rule.forced == 2       ? rule.narrow
                                                : choose_tile_rows(cu, cu_loop, nseq, heads, rule.wide, rule.narrow,
                                                                   rule.narrow_always, rule.max_loop, rule.penalty,
-                                                                  order, ncu);
+                                                                  order, ncu, &items);
     p->rule = rule;
     p->heads = heads;
     p->block = block;
     p->order = order;
     p->device = device;
     p->chunk = chunk;
-    std::vector<Item> items = build_worklist(cu, cu_loop, nseq, heads, block, order, chunk);
+    if (items.empty() || chunk > 0) items = build_worklist(cu, cu_loop, nseq, heads, block, order, chunk);
     p->n_items = static_cast<int>(items.size());
     if (chunk > 0) {
       const std::vector<Item> red = build_reduce_list(cu, cu_loop, nseq, heads, block, chunk);
@@ -225,32 +426,37 @@ class PlanCache {
       if (chunk > 0) std::fprintf(stderr, "; loops split at %d rows, %d split tiles", chunk, p->n_reduce);
       std::fprintf(stderr, "\n");
     }
-    if (bytes > 0 && fail_alloc_for_test()) return set_error(T2V_ERR_OOM, "hipMalloc of the work list failed (forced)");
     if (bytes > 0) {
-      e = hipMalloc(&p->d_items, bytes);
-      if (e != hipSuccess) {
-        (void)hipGetLastError();
-        return set_error(T2V_ERR_OOM, "hipMalloc of the work list failed");
+      DevicePools& dp = pools(device);
+      std::lock_guard<std::mutex> plock(dp.mu);
+      ListPool::Block staging;
+      if (int st = dp.dev.alloc(bytes, &p->mem)) return st;
+      if (int st = dp.pin.alloc(bytes, &staging)) {
+        dp.dev.release_after(p->mem, {});
+        p->mem = ListPool::Block{};
+        return st;
       }
-      e = hipHostMalloc(&p->h_items, bytes, hipHostMallocDefault);
+      p->d_items = static_cast<Item*>(p->mem.ptr);
+      std::memcpy(staging.ptr, items.data(), bytes);
+      e = hipMemcpyAsync(p->d_items, staging.ptr, bytes, hipMemcpyHostToDevice, stream);
+      hipEvent_t copied = nullptr;
+      if (e == hipSuccess) e = dp.pin.take_event(&copied);
+      if (e == hipSuccess) e = hipEventRecord(copied, stream);
       if (e != hipSuccess) {
-        (void)hipGetLastError();
-        return set_error(T2V_ERR_OOM, "hipHostMalloc of the work-list staging failed");
+        if (copied != nullptr) (void)hipEventDestroy(copied);
+        (void)hipStreamSynchronize(stream);  // the staging block may still be read
+        dp.pin.release_after(staging, {});
+        return hip_fail(e, "upload of the work list");
       }
-      std::memcpy(p->h_items, items.data(), bytes);
+      dp.pin.release_after(staging, {copied});
+      e = dp.dev.take_event(&p->ready);
+      if (e == hipSuccess) e = hipEventRecord(p->ready, stream);
+      if (e != hipSuccess) return hip_fail(e, "hipEventRecord of the work-list upload");
     }
-    e = hipEventCreateWithFlags(&p->ready, hipEventDisableTiming);
-    if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
-    if (bytes > 0) {
-      e = hipMemcpyAsync(p->d_items, p->h_items, bytes, hipMemcpyHostToDevice, stream);
-      if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync of the work list");
-    }
-    e = hipEventRecord(p->ready, stream);
-    if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
     plans_.push_front(p);
     *out = p;
-    // An evicted plan is freed (after its device finishes) when its last reference goes:
-    // here after the lock is released, or later by a call still holding it.
+    // An evicted plan's list returns to the pool (after its launches) when its last
+    // reference goes: here after the lock is released, or later by a call still holding it.
     while (plans_.size() > kMaxPlans) {
       evicted.push_back(std::move(plans_.back()));
       plans_.pop_back();
@@ -258,12 +464,14 @@ class PlanCache {
     return T2V_OK;
   }
 
+  // Waits for the device, then drops every plan and frees the pools' memory.
   void clear() {
     std::list<PlanRef> old;
     {
       std::lock_guard<std::mutex> lock(mu_);
       old.swap(plans_);
     }
+    old.clear();  // plans still referenced by a call in progress stay alive until it ends
   }
 
  private:
@@ -401,6 +609,7 @@ namespace {
 // Forward over queries at cu_q and keys at cu_k (the same array for self-attention).
 int attn_fwd_impl(const void* q, const void* k, const void* v, const int32_t* cu_q, const int32_t* cu_k, int nseq,
                   int heads, int head_dim, float scale, void* out, float* lse, void* stream) {
+  if (int st = check_offsets_on_host(cu_q, cu_k)) return st;
   int64_t Tq = 0, Tk = 0;
   if (cu_q == cu_k) {
     if (int st = validate_shape(cu_q, nseq, heads, head_dim, scale, &Tq)) return st;
@@ -413,9 +622,6 @@ int attn_fwd_impl(const void* q, const void* k, const void* v, const int32_t* cu
   const int64_t lb = Tq * heads * 4;
   if (int st = validate_pointers({{q, qb, "q"}, {k, kb, "k"}, {v, kb, "v"}}, {{out, qb, "out"}, {lse, lb, "lse"}}))
     return st;
-  if (int st = check_host_pointer(cu_q)) return st;
-  if (cu_k != cu_q)
-    if (int st = check_host_pointer(cu_k)) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   PlanRef plan;
   if (int st = cache().get(cu_q, cu_k, nseq, heads, fwd_rule(head_dim), order_from_env(), 0, s, &plan)) return st;
@@ -431,13 +637,15 @@ int attn_fwd_impl(const void* q, const void* k, const void* v, const int32_t* cu
   a.scale = scale;
   a.trace = tracer().reserve(plan->n_items);
   hipError_t e = timer().run(kSlotFwd, s, [&] { return launch_fwd(a, out, lse, plan->d_items, plan->n_items, s); });
+  const int used = note_use(plan, s);
   if (e != hipSuccess) return hip_fail(e, "forward kernel launch");
-  return T2V_OK;
+  return used;
 }
 
 int attn_bwd_impl(const void* q, const void* k, const void* v, const void* out, const float* lse, const int32_t* cu_q,
                   const int32_t* cu_k, int nseq, int heads, int head_dim, float scale, const void* dout, void* dq,
                   void* dk, void* dv, float* delta_ws, void* stream) {
+  if (int st = check_offsets_on_host(cu_q, cu_k)) return st;
   int64_t Tq = 0, Tk = 0;
   if (cu_q == cu_k) {
     if (int st = validate_shape(cu_q, nseq, heads, head_dim, scale, &Tq)) return st;
@@ -452,9 +660,6 @@ int attn_bwd_impl(const void* q, const void* k, const void* v, const void* out, 
           {{q, qb, "q"}, {k, kb, "k"}, {v, kb, "v"}, {out, qb, "out"}, {lse, lb, "lse"}, {dout, qb, "dout"}},
           {{dq, qb, "dq"}, {dk, kb, "dk"}, {dv, kb, "dv"}, {delta_ws, 2 * lb, "delta_ws"}}))
     return st;
-  if (int st = check_host_pointer(cu_q)) return st;
-  if (cu_k != cu_q)
-    if (int st = check_host_pointer(cu_k)) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int order = order_from_env();
   PlanRef pk, pq;
@@ -495,12 +700,16 @@ int attn_bwd_impl(const void* q, const void* k, const void* v, const void* out, 
       if (r == hipSuccess && pk->n_reduce > 0) r = launch_bwd_dkdv_reduce(a, pk->d_items + pk->n_items, pk->n_reduce, s);
       return r;
     });
+    const int used = note_use(pk, s);
     if (e != hipSuccess) return hip_fail(e, "dK/dV kernel launch");
+    if (used != T2V_OK) return used;
   }
   if (pq->n_items > 0) {
     a.trace = tracer().reserve(pq->n_items);
     e = timer().run(kSlotDq, s, [&] { return launch_bwd_dq(a, pq->d_items, pq->n_items, s); });
+    const int used = note_use(pq, s);
     if (e != hipSuccess) return hip_fail(e, "dQ kernel launch");
+    if (used != T2V_OK) return used;
   }
   return T2V_OK;
 }
@@ -587,6 +796,7 @@ int t2v_trace_count(int64_t* n_records, int* n_overflowed) {
 void t2v_release_cache(void) {
   (void)hipDeviceSynchronize();
   t2v::cache().clear();
+  t2v::trim_pools_after_sync();
 }
 
 }  // extern "C"

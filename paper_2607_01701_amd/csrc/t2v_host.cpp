@@ -13,6 +13,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <iterator>
 #include <numeric>
 #include <queue>
 
@@ -184,7 +185,8 @@ LoopSplit choose_loop_split(const int32_t* cu, const int32_t* cul, int nseq, int
 }
 
 int choose_tile_rows(const int32_t* cu, const int32_t* cul, int nseq, int heads, int wide, int narrow,
-                     bool narrow_always, double narrow_max_loop, double narrow_penalty, int order, int slots) {
+                     bool narrow_always, double narrow_max_loop, double narrow_penalty, int order, int slots,
+                     std::vector<Item>* chosen) {
   if (narrow_always) return narrow;
   double work = 0.0, weighted = 0.0;
   for (int s = 0; s < nseq; ++s) {
@@ -196,11 +198,13 @@ int choose_tile_rows(const int32_t* cu, const int32_t* cul, int nseq, int heads,
   if (work <= 0.0 || weighted <= narrow_max_loop * work) return narrow;
   if (slots < 1) return wide;
   double ms_wide = 0.0, ms_narrow = 0.0, lb = 0.0;
-  const std::vector<Item> w = build_worklist(cu, cul, nseq, heads, wide, order);
+  std::vector<Item> w = build_worklist(cu, cul, nseq, heads, wide, order);
   plan_makespan(w.data(), static_cast<int>(w.size()), wide, slots, &ms_wide, &lb);
-  const std::vector<Item> n = build_worklist(cu, cul, nseq, heads, narrow, order);
+  std::vector<Item> n = build_worklist(cu, cul, nseq, heads, narrow, order);
   plan_makespan(n.data(), static_cast<int>(n.size()), narrow, slots, &ms_narrow, &lb);
-  return ms_narrow * narrow_penalty < ms_wide ? narrow : wide;
+  const bool take_narrow = ms_narrow * narrow_penalty < ms_wide;
+  if (chosen != nullptr) *chosen = std::move(take_narrow ? n : w);
+  return take_narrow ? narrow : wide;
 }
 
 std::vector<Item> build_reduce_list(const int32_t* cu, const int32_t* cul, int nseq, int heads, int block,
@@ -296,6 +300,48 @@ std::vector<Item> build_worklist(const int32_t* cu, const int32_t* cu_loop, int 
   items.resize(n);
   for (size_t b = 0; b < n; ++b) items[b] = q[b % kNumXcd][b / kNumXcd];
   return items;
+}
+
+RangeAllocator::RangeAllocator(uint64_t size) : size_(size / kAlign * kAlign), free_total_(size_) {
+  if (size_ > 0) free_.push_back({0, size_});
+}
+
+int64_t RangeAllocator::alloc(uint64_t bytes) {
+  const uint64_t need = rounded(bytes == 0 ? 1 : bytes);
+  for (size_t i = 0; i < free_.size(); ++i) {
+    if (free_[i].second < need) continue;
+    const uint64_t off = free_[i].first;
+    free_[i].first += need;
+    free_[i].second -= need;
+    if (free_[i].second == 0) free_.erase(free_.begin() + static_cast<std::ptrdiff_t>(i));
+    free_total_ -= need;
+    return static_cast<int64_t>(off);
+  }
+  return -1;
+}
+
+bool RangeAllocator::release(uint64_t off, uint64_t bytes) {
+  const uint64_t len = rounded(bytes == 0 ? 1 : bytes);
+  if (off % kAlign != 0 || off > size_ || len > size_ - off) return false;
+  // First free range at or after off; the released range must fit between it and the one before.
+  auto it = std::lower_bound(free_.begin(), free_.end(), std::make_pair(off, uint64_t(0)));
+  if (it != free_.end() && it->first < off + len) return false;                         // overlaps a free range
+  if (it != free_.begin() && std::prev(it)->first + std::prev(it)->second > off) return false;
+  it = free_.insert(it, {off, len});
+  free_total_ += len;
+  auto next = std::next(it);
+  if (next != free_.end() && it->first + it->second == next->first) {  // merge with the next range
+    it->second += next->second;
+    it = std::prev(free_.erase(next));
+  }
+  if (it != free_.begin()) {  // merge with the previous range
+    auto prev = std::prev(it);
+    if (prev->first + prev->second == it->first) {
+      prev->second += it->second;
+      free_.erase(it);
+    }
+  }
+  return true;
 }
 
 void plan_makespan(const Item* items, int n, int block, int slots, double* makespan, double* lower_bound) {

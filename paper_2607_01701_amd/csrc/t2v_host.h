@@ -5,6 +5,7 @@
 
 #include <cstdint>
 #include <string>
+#include <utility>
 #include <vector>
 
 namespace t2v {
@@ -85,14 +86,37 @@ LoopSplit choose_loop_split(const int32_t* cu_own, const int32_t* cu_loop, int n
 // length L'); otherwise narrow only when the list-scheduling makespan of the narrow work list
 // over `slots` workers, times narrow_penalty (the narrow kernel's measured cost per unit of
 // work relative to the wide one on long loops), is below the wide list's: few tiles per CU
-// leave the last round of wide tiles part-empty.
+// leave the last round of wide tiles part-empty. When both lists were built for the
+// comparison and `chosen` is given, the chosen one is moved into it (else it is left empty).
 int choose_tile_rows(const int32_t* cu_own, const int32_t* cu_loop, int nseq, int heads, int wide, int narrow,
-                     bool narrow_always, double narrow_max_loop, double narrow_penalty, int order, int slots);
+                     bool narrow_always, double narrow_max_loop, double narrow_penalty, int order, int slots,
+                     std::vector<Item>* chosen = nullptr);
 
 // One item per split tile of build_worklist(..., chunk): row0, len, tile0, head of the tile,
 // slot = its first partial slot, pieces = the number of consecutive slots to sum.
 std::vector<Item> build_reduce_list(const int32_t* cu_own, const int32_t* cu_loop, int nseq, int heads, int block,
                                     int chunk);
+
+// First-fit allocator of byte ranges inside one memory chunk of `size` bytes (host-side
+// bookkeeping only: the chunk itself is device or pinned host memory owned by the caller).
+// Sizes are rounded up to kAlign; freed neighbours coalesce.
+class RangeAllocator {
+ public:
+  static constexpr uint64_t kAlign = 256;
+  explicit RangeAllocator(uint64_t size = 0);
+  uint64_t size() const { return size_; }
+  // Offset of a free range of at least `bytes` (rounded up), or -1 when none is large enough.
+  int64_t alloc(uint64_t bytes);
+  // Returns a range obtained from alloc (same `bytes`); false if it is not a live range.
+  bool release(uint64_t off, uint64_t bytes);
+  uint64_t free_bytes() const { return free_total_; }
+  size_t free_ranges() const { return free_.size(); }
+  static uint64_t rounded(uint64_t bytes) { return (bytes + kAlign - 1) / kAlign * kAlign; }
+
+ private:
+  uint64_t size_ = 0, free_total_ = 0;
+  std::vector<std::pair<uint64_t, uint64_t>> free_;  // (offset, length), sorted by offset, disjoint
+};
 
 // Greedy list-scheduling makespan of `items` on `slots` workers, dealt per XCD when
 // slots is a multiple of kNumXcd. Costs are tile rows x looped-over length.

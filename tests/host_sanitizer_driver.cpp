@@ -1,5 +1,5 @@
 // Randomised exercise of the host-side code of libt2vattn (tile scheduler and its loop
-// split, makespan model, argument validation, cascade planner), built with AddressSanitizer and
+// split, makespan model, argument validation, cascade planner, work-list pool allocator), built with AddressSanitizer and
 // UndefinedBehaviorSanitizer by tests/test_host_sanitizers.py. Every check that fails prints
 // a line; the exit status is the number of failed checks (sanitizer reports abort earlier).
 #include <algorithm>
@@ -268,8 +268,66 @@ static void planner(std::mt19937& rng) {
             T2V_ERR_INVALID_ARG, "cycle refused");
 }
 
+// The work-list memory pool's range allocator against a byte-map model: every allocation
+// is disjoint from every live one and inside the chunk, double or foreign releases are
+// refused, the free byte count is exact, and freeing everything leaves one range.
+static void range_allocator(std::mt19937& rng) {
+  for (int rep = 0; rep < 40; ++rep) {
+    const uint64_t size = t2v::RangeAllocator::kAlign * std::uniform_int_distribution<uint64_t>(1, 400)(rng);
+    t2v::RangeAllocator a(size);
+    std::vector<int> owner(size / t2v::RangeAllocator::kAlign, -1);  // allocation id per 256-byte unit
+    std::vector<std::pair<uint64_t, uint64_t>> live;                 // (offset, bytes)
+    for (int op = 0; op < 600; ++op) {
+      if (live.empty() || std::uniform_int_distribution<int>(0, 2)(rng) > 0) {
+        const uint64_t bytes = std::uniform_int_distribution<uint64_t>(0, 9000)(rng);
+        const int64_t off = a.alloc(bytes);
+        const uint64_t units = t2v::RangeAllocator::rounded(bytes == 0 ? 1 : bytes) / t2v::RangeAllocator::kAlign;
+        if (off < 0) {  // refused: no free run of that many units (first fit scans all of them)
+          uint64_t run = 0, best = 0;
+          for (int o : owner) {
+            run = o < 0 ? run + 1 : 0;
+            best = std::max(best, run);
+          }
+          CHECK(best < units, "allocation refused although a free run exists");
+          continue;
+        }
+        CHECK(static_cast<uint64_t>(off) % t2v::RangeAllocator::kAlign == 0, "aligned offset");
+        const uint64_t u0 = static_cast<uint64_t>(off) / t2v::RangeAllocator::kAlign;
+        CHECK(u0 + units <= owner.size(), "allocation inside the chunk");
+        for (uint64_t u = u0; u < u0 + units && u < owner.size(); ++u) {
+          CHECK(owner[u] < 0, "allocation disjoint from live ones");
+          owner[u] = static_cast<int>(live.size());
+        }
+        live.push_back({static_cast<uint64_t>(off), bytes});
+      } else {
+        const size_t i = std::uniform_int_distribution<size_t>(0, live.size() - 1)(rng);
+        const auto r = live[i];
+        CHECK(a.release(r.first, r.second), "release of a live range");
+        CHECK(!a.release(r.first, r.second), "double release refused");
+        const uint64_t units = t2v::RangeAllocator::rounded(r.second == 0 ? 1 : r.second) / t2v::RangeAllocator::kAlign;
+        for (uint64_t u = r.first / t2v::RangeAllocator::kAlign; u < r.first / t2v::RangeAllocator::kAlign + units; ++u)
+          owner[u] = -1;
+        live.erase(live.begin() + static_cast<std::ptrdiff_t>(i));
+        for (size_t j = 0; j < live.size(); ++j) {  // renumber owners after the erase
+          const uint64_t n = t2v::RangeAllocator::rounded(live[j].second == 0 ? 1 : live[j].second) /
+                             t2v::RangeAllocator::kAlign;
+          for (uint64_t u = live[j].first / t2v::RangeAllocator::kAlign; u < live[j].first / t2v::RangeAllocator::kAlign + n; ++u)
+            owner[u] = static_cast<int>(j);
+        }
+      }
+      uint64_t free_units = 0;
+      for (int o : owner) free_units += o < 0 ? 1 : 0;
+      CHECK(a.free_bytes() == free_units * t2v::RangeAllocator::kAlign, "free byte count");
+    }
+    CHECK(!a.release(size, 256), "release past the chunk refused");
+    for (const auto& r : live) CHECK(a.release(r.first, r.second), "final release");
+    CHECK(a.free_bytes() == a.size() && a.free_ranges() == (a.size() > 0 ? 1u : 0u), "everything coalesces");
+  }
+}
+
 int main() {
   std::mt19937 rng(20260);
+  range_allocator(rng);
   worklists(rng);
   loop_split(rng);
   tile_choice();

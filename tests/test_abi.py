@@ -268,3 +268,85 @@ def test_header_is_plain_c_and_links(tmp_path, lib):
     assert r.returncode == 0, (r.returncode, r.stdout, r.stderr)
     assert "libt2vattn" in r.stdout
     assert ("NULL" if lib == "t2vattn" else "cu_seqlens") in r.stdout  # the refused call's message
+
+
+# ----------------------------------------------------------------- torch binding checks
+#
+# The C ABI sees only pointers, so the torch wrappers check every tensor's shape, dtype and
+# layout, and that cu_seqlens ends at the packed row count, before anything is launched.
+# These run on CPU tensors: the shape, dtype and layout checks come before the device check.
+
+def _cpu(shape, dtype=None):
+    import torch
+    return torch.zeros(shape, dtype=torch.bfloat16 if dtype is None else dtype)
+
+
+@pytest.mark.parametrize("case,msg", [
+    ("cu_short", "does not match the 10 rows"),
+    ("cu_long", "does not match the 10 rows"),
+    ("out_shape", "out has shape"),
+    ("lse_dtype", "lse has dtype"),
+    ("lse_shape", "lse has shape"),
+    ("q_noncontig", "q must be contiguous"),
+    ("cpu_tensor", "must be a CUDA tensor"),
+])
+def test_attn_fwd_wrapper_rejects_before_launch(case, msg):
+    import torch
+    from paper_2607_01701_amd import attn_fwd
+    T, H, D = 10, 2, 64
+    q, k, v = _cpu((T, H, D)), _cpu((T, H, D)), _cpu((T, H, D))
+    cu, kw = [0, 4, 10], {}
+    if case == "cu_short":
+        cu = [0, 4, 9]
+    elif case == "cu_long":
+        cu = [0, 4, 11]
+    elif case == "out_shape":
+        kw["out"] = _cpu((T + 1, H, D))
+    elif case == "lse_dtype":
+        kw["lse"] = _cpu((H, T), torch.bfloat16)
+    elif case == "lse_shape":
+        kw["lse"] = _cpu((T, H), torch.float32)
+    elif case == "q_noncontig":
+        q = _cpu((T, D, H)).transpose(1, 2)
+    with pytest.raises(ValueError, match=msg):
+        attn_fwd(q, k, v, cu, 0.125, **kw)
+
+
+@pytest.mark.parametrize("case,msg", [
+    ("cu_short", "does not match the 10 rows"),
+    ("cu_k_short", "cu_seqlens_k.* does not match the 6 rows"),
+    ("dq_shape", "dq has shape"),
+    ("dk_shape", "dk has shape"),
+    ("dv_dtype", "dv has dtype"),
+    ("ws_shape", "delta_ws has shape"),
+    ("ws_dtype", "delta_ws has dtype"),
+    ("lse_shape", "lse has shape"),
+])
+def test_attn_bwd_wrapper_rejects_before_launch(case, msg):
+    import torch
+    from paper_2607_01701_amd import attn_bwd
+    T, Tk, H, D = 10, 6, 2, 64
+    cross = case == "cu_k_short"
+    nk = Tk if cross else T
+    q, out, g = _cpu((T, H, D)), _cpu((T, H, D)), _cpu((T, H, D))
+    k, v = _cpu((nk, H, D)), _cpu((nk, H, D))
+    lse = _cpu((H, T), torch.float32)
+    cu, kw = [0, 4, 10], {}
+    if cross:
+        kw["cu_seqlens_k"] = [0, 2, 5]
+    if case == "cu_short":
+        cu = [0, 4, 8]
+    elif case == "dq_shape":
+        kw["dq"] = _cpu((T, H, D + 1))
+    elif case == "dk_shape":
+        kw["dk"] = _cpu((T - 1, H, D))
+    elif case == "dv_dtype":
+        kw["dv"] = _cpu((T, H, D), torch.float16)
+    elif case == "ws_shape":
+        kw["delta_ws"] = _cpu((H, T), torch.float32)  # [H, T]: half of what the library writes
+    elif case == "ws_dtype":
+        kw["delta_ws"] = _cpu((2, H, T), torch.bfloat16)
+    elif case == "lse_shape":
+        lse = _cpu((H, T + 1), torch.float32)
+    with pytest.raises(ValueError, match=msg):
+        attn_bwd(q, k, v, out, lse, g, cu, 0.125, **kw)

@@ -112,3 +112,80 @@ def test_forced_allocation_failure_is_reported_and_recovers(monkeypatch):
     o2, _ = attn_fwd(d["q"], d["k"], d["v"], pack.cu_seqlens, pack.scale)
     torch.cuda.synchronize()
     assert torch.equal(o1, o2)
+
+
+def test_fresh_packs_on_concurrent_streams_reuse_list_memory():
+    """Work-list memory is recycled while kernels on other streams still run: four threads,
+    each on its own stream, call fwd + bwd on 30 packs no other call uses (360 work lists
+    through a cache of 64, so lists are released and their memory handed to new ones while
+    launches are in flight). Every result must equal the same call made alone. All buffers
+    are sized for the largest pack, so even a list overwritten too early would stay inside
+    them (and show up as a wrong result, not a fault)."""
+    import ctypes
+    import torch
+    from paper_2607_01701_amd import _lib
+    rng = np.random.default_rng(123)
+    n_threads, per = 4, 30
+    H, D = 2, 128
+    packs = [[int(x) for x in rng.integers(1, 700, size=int(rng.integers(1, 5)))] for _ in range(n_threads * per)]
+    tmax = max(sum(p) for p in packs)
+    gen = torch.Generator(device="cuda").manual_seed(5)
+    q, k, v, g = (torch.randn((tmax, H, D), generator=gen, device="cuda").to(torch.bfloat16) for _ in range(4))
+    L = _lib.lib()
+    sc = 1.0 / D ** 0.5
+
+    def call(lengths, bufs, stream):
+        cu = np.ascontiguousarray(np.concatenate([[0], np.cumsum(lengths)]), dtype=np.int32)
+        cp = cu.ctypes.data_as(_lib._i32p)
+        n = len(lengths)
+        s = stream.cuda_stream
+        st = L.t2v_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), cp, n, H, D, sc, bufs["out"].data_ptr(),
+                            bufs["lse"].data_ptr(), s)
+        assert st == 0, _lib.t2v_last_error(L)
+        st = L.t2v_attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), bufs["out"].data_ptr(), bufs["lse"].data_ptr(),
+                            cp, n, H, D, sc, g.data_ptr(), bufs["dq"].data_ptr(), bufs["dk"].data_ptr(),
+                            bufs["dv"].data_ptr(), bufs["ws"].data_ptr(), s)
+        assert st == 0, _lib.t2v_last_error(L)
+        T = int(cu[-1])
+        # lse is [H, T] for this call's T: its first H * T floats (not a [:, :T] slice).
+        return {"out": bufs["out"][:T].clone(), "dq": bufs["dq"][:T].clone(), "dk": bufs["dk"][:T].clone(),
+                "dv": bufs["dv"][:T].clone(), "lse": bufs["lse"].view(-1)[:H * T].view(H, T).clone()}
+
+    def buffers():
+        b = {n: torch.zeros((tmax, H, D), dtype=torch.bfloat16, device="cuda") for n in ("out", "dq", "dk", "dv")}
+        b["lse"] = torch.zeros((H, tmax), dtype=torch.float32, device="cuda")
+        b["ws"] = torch.zeros((2, H, tmax), dtype=torch.float32, device="cuda")
+        return b
+
+    log(f"case {n_threads} threads x {per} fresh packs (alone first)")
+    main = torch.cuda.current_stream()
+    b0 = buffers()
+    alone = []
+    for p in packs:
+        alone.append(call(p, b0, main))
+    torch.cuda.synchronize()
+    _lib.t2v_release_cache()  # the threaded calls all miss the cache
+    results, errors = [None] * len(packs), []
+
+    def worker(t):
+        try:
+            st = torch.cuda.Stream()
+            with torch.cuda.stream(st):  # buffers filled on the same stream as the calls that write them
+                bufs = buffers()
+                for j in range(per):
+                    i = t * per + j
+                    results[i] = call(packs[i], bufs, st)
+            st.synchronize()
+        except Exception as e:  # reported below
+            errors.append(repr(e))
+
+    threads = [threading.Thread(target=worker, args=(t,)) for t in range(n_threads)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=300)
+    assert not any(t.is_alive() for t in threads), "a worker thread did not finish"
+    assert not errors, errors
+    torch.cuda.synchronize()
+    bad = [i for i in range(len(packs)) if not same(alone[i], results[i])]
+    assert not bad, f"{len(bad)} packs differ from their single-stream result, first {packs[bad[0]]}"

@@ -1,11 +1,18 @@
 """Parity at the full sizes of the four large workloads, in the launch configuration the
 benchmark times (same entry points, same work lists, default scheduler order).
 
-The full float64 oracle is O(L^2) per clip and head, so these tests compare, element by
-element, what the oracle computes one by one: out / lse / dq at sampled (token, head) rows;
-dk / dv at sampled keys of one head of a clip (the oracle needs that head's full forward);
-the complete outputs of short clips. Properties that hold at any size are checked for every
-(clip, head): sum_j dk_j = 0, sum_j dv_j = sum_i dout_i, <Q, dQ> = <K, dK>.
+The tolerance gate (relative max error over the whole packed tensor, 2e-2 for out, dq, dk,
+dv; 1e-3 absolute for lse) is computed on:
+* uniform: the full oracle, every clip and head, whole tensors;
+* hetero: the full oracle on the head subset {0, H/2, H-1} over every clip (heads are
+  independent, so the subset is exact for those heads), whole tensors restricted to them,
+  plus the per-clip errors, each held to the same bound;
+* long and skew (75,600- and 100,800-token clips, where one head alone is ~10^10 scores):
+  dk and dv for every key of one head of the long clip (the oracle forms that head's whole
+  backward), out / lse / dq at sampled rows of every head, and the complete outputs of the
+  short clips.
+Properties that hold at any size are checked for every (clip, head): sum_j dk_j = 0,
+sum_j dv_j = sum_i dout_i, <Q, dQ> = <K, dK>.
 """
 import numpy as np
 import pytest
@@ -105,22 +112,54 @@ def check_query_rows(name):
     assert e_out <= TOL_REL and e_dq <= TOL_REL and e_lse <= TOL_LSE
 
 
+def check_full_oracle(name, heads=None):
+    """The whole-tensor gate against the full oracle (all heads, or a head subset over every
+    clip), with the per-clip errors logged and held to the same bound."""
+    from gpu_util import compare_full
+    pack, res = workload_run(name)
+    hs = list(range(pack.heads)) if heads is None else list(heads)
+    log(f"{name}: full oracle on every clip, heads {hs if heads is not None else 'all'}")
+    sl = {n: f64(getattr(pack, n)[:, hs]) for n in ("q", "k", "v", "dout")}
+    ref = oracle.attention(sl["q"], sl["k"], sl["v"], sl["dout"], pack.cu_seqlens, pack.scale)
+    hidx = np.asarray(hs)
+    got = {k: res[k][:, hidx].double().cpu().numpy() for k in ("out", "dq", "dk", "dv")}
+    got["lse"] = res["lse"][hidx].double().cpu().numpy()
+    errs, worst = compare_full(got, ref, pack.cu_seqlens, label=f"{name} heads {len(hs)}")
+    for k in ("out", "dq", "dk", "dv"):
+        assert errs[k] <= TOL_REL, (k, errs[k])
+        assert worst[k] <= TOL_REL, (k, "per clip", worst[k])
+    assert errs["lse"] <= TOL_LSE, errs["lse"]
+
+
 def check_key_rows(name, seq, head, nkeys=12, torch_backend=False):
+    """dk / dv of one (clip, head) at sampled keys, or at every key (nkeys=None)."""
     pack, res = workload_run(name)
     cu = pack.cu_seqlens
     a, b = int(cu[seq]), int(cu[seq + 1])
     L = b - a
     rng = np.random.default_rng(2)
-    keys = sorted(set([0, 1, 127, 128, L - 2, L - 1] + list(rng.integers(0, L, nkeys))))
+    if nkeys is None:
+        keys = list(range(L))
+    else:
+        keys = sorted(set([0, 1, 127, 128, L - 2, L - 1] + list(rng.integers(0, L, nkeys))))
     log(f"{name}: oracle dk/dv on clip {seq} (L={L}) head {head}, {len(keys)} keys")
     sl = {n: slice_head(pack, n, a, b, head)[:, None, :] for n in ("q", "k", "v", "dout")}
-    fn = oracle.key_rows_torch if torch_backend else oracle.key_rows
-    ref = fn(sl["q"], sl["k"], sl["v"], sl["dout"], np.array([0, L]), pack.scale, 0, 0, keys)
+    if torch_backend:
+        step = max(1, L // 8)
+
+        def progress(r1, n):
+            if r1 // step != (r1 - 2048) // step or r1 == n:
+                log(f"{name}: oracle query rows {r1}/{n}")
+
+        ref = oracle.key_rows_torch(sl["q"], sl["k"], sl["v"], sl["dout"], np.array([0, L]), pack.scale, 0, 0, keys,
+                                    progress=progress)
+    else:
+        ref = oracle.key_rows(sl["q"], sl["k"], sl["v"], sl["dout"], np.array([0, L]), pack.scale, 0, 0, keys)
     toks = [a + j for j in keys]
     hs = [head] * len(keys)
     e_dk = np.max(np.abs(gpu_rows(res["dk"], toks, hs) - ref["dk"])) / np.max(np.abs(ref["dk"]))
     e_dv = np.max(np.abs(gpu_rows(res["dv"], toks, hs) - ref["dv"])) / np.max(np.abs(ref["dv"]))
-    log(f"{name}: sampled keys dk {e_dk:.3e} dv {e_dv:.3e}")
+    log(f"{name}: {'all' if nkeys is None else 'sampled'} keys dk {e_dk:.3e} dv {e_dv:.3e}")
     assert e_dk <= TOL_REL and e_dv <= TOL_REL
 
 
@@ -179,19 +218,17 @@ def check_invariants(name):
 
 @pytest.mark.timeout(600)
 def test_full_size_uniform():
-    check_query_rows("uniform")
+    check_full_oracle("uniform")
     check_invariants("uniform")
-    check_short_clips("uniform", 4096, max_clips=1, heads=[0, 11, 23])
-    check_key_rows("uniform", seq=3, head=7)
 
 
 @pytest.mark.timeout(600)
 def test_full_size_hetero():
+    pack, _ = workload_run("hetero")
+    check_full_oracle("hetero", heads=[0, pack.heads // 2, pack.heads - 1])
     check_query_rows("hetero")
     check_invariants("hetero")
-    check_short_clips("hetero", 1280, max_clips=1)
-    pack, _ = workload_run("hetero")
-    check_key_rows("hetero", seq=int(np.argmax(np.diff(pack.cu_seqlens))), head=5)
+    check_key_rows("hetero", seq=int(np.argmax(np.diff(pack.cu_seqlens))), head=5, nkeys=None)
 
 
 @pytest.mark.timeout(900)
@@ -199,7 +236,7 @@ def test_full_size_long():
     check_query_rows("long")
     check_invariants("long")
     pack, _ = workload_run("long")
-    check_key_rows("long", seq=0, head=pack.heads // 2, nkeys=6, torch_backend=True)
+    check_key_rows("long", seq=0, head=pack.heads // 2, nkeys=None, torch_backend=True)
 
 
 @pytest.mark.timeout(900)
@@ -208,5 +245,5 @@ def test_full_size_skew():
     check_invariants("skew")
     check_short_clips("skew", 1024, max_clips=2)
     pack, _ = workload_run("skew")
-    check_key_rows("skew", seq=int(np.argmax(np.diff(pack.cu_seqlens))), head=pack.heads // 2, nkeys=6,
+    check_key_rows("skew", seq=int(np.argmax(np.diff(pack.cu_seqlens))), head=pack.heads // 2, nkeys=None,
                    torch_backend=True)
