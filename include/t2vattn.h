@@ -119,6 +119,24 @@ int t2v_attn_bwd(const void* q, const void* k, const void* v,
                  const void* dout, void* dq, void* dk, void* dv, float* delta_ws,
                  void* stream);
 
+/* Backward pass that allocates nothing, for callers that cannot allocate device memory
+ * (code under stream capture, tight serving loops, harnesses that forbid allocation).
+ * Arguments, results and errors are those of t2v_attn_bwd without delta_ws: the Delta / lse
+ * scratch (8 * heads * T bytes) and the dK/dV and dQ work lists (32 bytes per work item,
+ * built on the host at every call, not cached) are kept in one static 64 MiB device array
+ * of the library, one per GPU, held until the process ends. No hipMalloc, hipHostMalloc or
+ * other device allocation is made; the work lists are copied from host memory with
+ * hipMemcpyAsync on `stream`, which for a pageable source makes the call wait for that copy.
+ *   Limit: a call needing more than 64 MiB (8 * heads * T plus the lists: about
+ *   heads * T <= 8e6 tokens x heads) returns T2V_ERR_INVALID_ARG before any launch.
+ *   Every call on a GPU shares the array: calls on one stream are ordered by it, but calls
+ *   that overlap on one GPU (other streams, other threads) race and must not be made.
+ * Results are bitwise equal to t2v_attn_bwd's for the same inputs. */
+int t2v_attn_bwd_noalloc(const void* q, const void* k, const void* v,
+                         const void* out, const float* lse,
+                         const int32_t* cu_seqlens, int nseq, int heads, int head_dim, float scale,
+                         const void* dout, void* dq, void* dk, void* dv, void* stream);
+
 /* Cross-attention: queries and keys from separate token streams, e.g. a clip's video tokens
  * attending to its text tokens. The paper's Wan2.1 model uses self- and cross-attention
  * (Section V-A), the DiT is conditioned on text (Section II-A), and text sequences are short,

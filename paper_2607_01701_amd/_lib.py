@@ -30,7 +30,7 @@ ORDER_LONGEST_FIRST = 1
 EXPORTS = ("t2v_attn_fwd", "t2v_attn_bwd", "t2v_attn_fwd_qk", "t2v_attn_bwd_qk", "t2v_last_error",
            "t2v_release_cache", "t2v_build_worklist", "t2v_plan_makespan", "t2v_timing_enable", "t2v_kernel_times",
            "t2v_version", "t2v_list_schedule", "t2v_plan_cascades", "t2v_probe_mfma_peak", "t2v_trace_set",
-           "t2v_trace_count")
+           "t2v_trace_count", "t2v_attn_bwd_noalloc")
 KERNEL_SLOTS = ("fwd", "bwd_pre", "bwd_dkdv", "bwd_dq")
 HOST_EXPORTS = ("t2v_last_error", "t2v_build_worklist", "t2v_plan_makespan", "t2v_version", "t2v_list_schedule",
                 "t2v_plan_cascades")
@@ -71,6 +71,9 @@ def _declare(lib, full: bool):
         lib.t2v_attn_bwd.restype = ctypes.c_int
         lib.t2v_attn_bwd.argtypes = [_vp, _vp, _vp, _vp, _f32p, _i32p, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                      ctypes.c_float, _vp, _vp, _vp, _vp, _f32p, _vp]
+        lib.t2v_attn_bwd_noalloc.restype = ctypes.c_int
+        lib.t2v_attn_bwd_noalloc.argtypes = [_vp, _vp, _vp, _vp, _f32p, _i32p, ctypes.c_int, ctypes.c_int,
+                                             ctypes.c_int, ctypes.c_float, _vp, _vp, _vp, _vp, _vp]
         lib.t2v_attn_fwd_qk.restype = ctypes.c_int
         lib.t2v_attn_fwd_qk.argtypes = [_vp, _vp, _vp, _i32p, _i32p, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                         ctypes.c_float, _vp, _f32p, _vp]
@@ -142,6 +145,13 @@ def t2v_attn_bwd(q, k, v, out, lse, cu_seqlens, nseq, heads, head_dim, scale, do
     cu = _cu_array(cu_seqlens)
     return lib().t2v_attn_bwd(q, k, v, out, lse, cu.ctypes.data_as(_i32p), nseq, heads, head_dim, scale, dout,
                               dq, dk, dv, delta_ws, stream)
+
+
+def t2v_attn_bwd_noalloc(q, k, v, out, lse, cu_seqlens, nseq, heads, head_dim, scale, dout, dq, dk, dv, stream):
+    """Direct call of t2v_attn_bwd_noalloc with integer addresses; returns the status."""
+    cu = _cu_array(cu_seqlens)
+    return lib().t2v_attn_bwd_noalloc(q, k, v, out, lse, cu.ctypes.data_as(_i32p), nseq, heads, head_dim, scale,
+                                      dout, dq, dk, dv, stream)
 
 
 def t2v_attn_fwd_qk(q, k, v, cu_seqlens_q, cu_seqlens_k, nseq, heads, head_dim, scale, out, lse, stream):

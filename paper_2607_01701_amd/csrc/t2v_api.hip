@@ -16,6 +16,11 @@
 #include "t2v_host.h"
 #include "t2v_kernels.h"
 
+// The no-allocation backward's scratch (see attn_bwd_noalloc_impl): one per GPU, held until
+// the process ends. Host code must not use this name as a device address.
+constexpr size_t kNoAllocScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
 namespace t2v {
 namespace {
 
@@ -714,6 +719,131 @@ int attn_bwd_impl(const void* q, const void* k, const void* v, const void* out, 
   return T2V_OK;
 }
 
+// ------------------------------------------------------------ backward without allocation
+//
+// For callers that cannot allocate device memory: the [2, H, T] Delta / lse scratch and
+// both work lists live in one static device array, `scratch`, instead of the caller's
+// delta_ws and the library's list pool. Its device address is taken once per GPU (with
+// that GPU current) and kept; host code uses only that address, never the array's name.
+// Every call on a GPU shares the array, so calls that overlap on one GPU (different
+// streams, or threads) race; calls on one stream are ordered by it. Nothing in it needs
+// to start at zero: each call overwrites the parts it reads (the Delta pass writes the
+// scratch rows, the list uploads the items).
+constexpr size_t kScratchAlign = 256;
+
+size_t align_up(size_t n) { return (n + kScratchAlign - 1) / kScratchAlign * kScratchAlign; }
+
+int scratch_address(int device, unsigned char** out) {
+  static std::mutex* mu = new std::mutex();
+  static std::vector<unsigned char*>* ptrs = new std::vector<unsigned char*>();  // never destroyed
+  std::lock_guard<std::mutex> lock(*mu);
+  if (device >= static_cast<int>(ptrs->size())) ptrs->resize(device + 1, nullptr);
+  if ((*ptrs)[device] == nullptr) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr) {
+      (void)hipGetLastError();
+      return set_error(T2V_ERR_HIP, std::string("hipGetSymbolAddress of the no-allocation scratch: ") +
+                                        hipGetErrorString(e));
+    }
+    (*ptrs)[device] = static_cast<unsigned char*>(p);
+  }
+  *out = (*ptrs)[device];
+  return T2V_OK;
+}
+
+int attn_bwd_noalloc_impl(const void* q, const void* k, const void* v, const void* out, const float* lse,
+                          const int32_t* cu, int nseq, int heads, int head_dim, float scale, const void* dout,
+                          void* dq, void* dk, void* dv, void* stream) {
+  if (int st = check_offsets_on_host(cu, cu)) return st;
+  int64_t T = 0;
+  if (int st = validate_shape(cu, nseq, heads, head_dim, scale, &T)) return st;
+  if (T == 0) return T2V_OK;
+  const int64_t tb = tensor_bytes(T, heads, head_dim), lb = T * heads * 4;
+  if (int st = validate_pointers(
+          {{q, tb, "q"}, {k, tb, "k"}, {v, tb, "v"}, {out, tb, "out"}, {lse, lb, "lse"}, {dout, tb, "dout"}},
+          {{dq, tb, "dq"}, {dk, tb, "dk"}, {dv, tb, "dv"}}))
+    return st;
+  const size_t delta_bytes = align_up(static_cast<size_t>(2 * lb));
+  auto too_big = [&](size_t need) {
+    return set_error(T2V_ERR_INVALID_ARG,
+                     "the no-allocation backward needs " + std::to_string(need) + " bytes of scratch (8 * heads * T "
+                     "for Delta and lse, 32 per work item), more than its " +
+                     std::to_string(kNoAllocScratchBytes) + "-byte array");
+  };
+  if (delta_bytes > kNoAllocScratchBytes) return too_big(delta_bytes);
+  // The same work lists as t2v_attn_bwd (tile rules, order, loop split), built per call.
+  const int order = order_from_env();
+  const int kv_rows = dkdv_tile_rows(head_dim);
+  const int ncu = cu_count();
+  int chunk = 0;
+  if (split_enabled()) chunk = choose_loop_split(cu, cu, nseq, heads, kv_rows, ncu, tb / dkdv_partial_slot_bytes(head_dim)).chunk;
+  std::vector<Item> kv = build_worklist(cu, cu, nseq, heads, kv_rows, order, chunk);
+  const int n_kv = static_cast<int>(kv.size());
+  int n_reduce = 0;
+  if (chunk > 0) {
+    const std::vector<Item> red = build_reduce_list(cu, cu, nseq, heads, kv_rows, chunk);
+    n_reduce = static_cast<int>(red.size());
+    kv.insert(kv.end(), red.begin(), red.end());
+  }
+  const TileRule qr = dq_rule(head_dim);
+  std::vector<Item> ql;
+  const int q_rows = qr.forced == 1   ? qr.wide
+                     : qr.forced == 2 ? qr.narrow
+                                      : choose_tile_rows(cu, cu, nseq, heads, qr.wide, qr.narrow, qr.narrow_always,
+                                                         qr.max_loop, qr.penalty, order, ncu, &ql);
+  if (ql.empty()) ql = build_worklist(cu, cu, nseq, heads, q_rows, order);
+  const size_t kv_bytes = align_up(kv.size() * sizeof(Item)), q_bytes = align_up(ql.size() * sizeof(Item));
+  if (delta_bytes + kv_bytes + q_bytes > kNoAllocScratchBytes) return too_big(delta_bytes + kv_bytes + q_bytes);
+  int device = 0;
+  hipError_t e = hipGetDevice(&device);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  unsigned char* base = nullptr;
+  if (int st = scratch_address(device, &base)) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Item* d_kv = reinterpret_cast<Item*>(base + delta_bytes);
+  Item* d_q = reinterpret_cast<Item*>(base + delta_bytes + kv_bytes);
+  // Pageable sources: the runtime stages them itself, in stream order (the call returns once
+  // the host arrays may be released).
+  if (!kv.empty()) e = hipMemcpyAsync(d_kv, kv.data(), kv.size() * sizeof(Item), hipMemcpyHostToDevice, s);
+  if (e == hipSuccess && !ql.empty()) e = hipMemcpyAsync(d_q, ql.data(), ql.size() * sizeof(Item), hipMemcpyHostToDevice, s);
+  if (e != hipSuccess) return hip_fail(e, "upload of the work lists into the no-allocation scratch");
+  AttnArgs a{};
+  a.q_rows = q_rows;
+  a.partial = static_cast<float*>(dq);
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.out = out;
+  a.lse = lse;
+  a.dout = dout;
+  a.dq = dq;
+  a.dk = dk;
+  a.dv = dv;
+  a.delta = reinterpret_cast<float*>(base);
+  a.heads = heads;
+  a.head_dim = head_dim;
+  a.total_tokens = T;
+  a.scale = scale;
+  e = timer().run(kSlotPre, s, [&] { return launch_bwd_pre(a, s); });
+  if (e != hipSuccess) return hip_fail(e, "backward preprocess launch");
+  if (n_kv > 0) {
+    a.trace = tracer().reserve(n_kv);
+    e = timer().run(kSlotDkdv, s, [&] {
+      hipError_t r = launch_bwd_dkdv(a, d_kv, n_kv, s);
+      if (r == hipSuccess && n_reduce > 0) r = launch_bwd_dkdv_reduce(a, d_kv + n_kv, n_reduce, s);
+      return r;
+    });
+    if (e != hipSuccess) return hip_fail(e, "dK/dV kernel launch");
+  }
+  if (!ql.empty()) {
+    a.trace = tracer().reserve(static_cast<int64_t>(ql.size()));
+    e = timer().run(kSlotDq, s, [&] { return launch_bwd_dq(a, d_q, static_cast<int>(ql.size()), s); });
+    if (e != hipSuccess) return hip_fail(e, "dQ kernel launch");
+  }
+  return T2V_OK;
+}
+
 // Runs f, turning host exceptions into statuses (none may cross the C ABI).
 template <typename F>
 int guarded(F&& f) {
@@ -744,6 +874,15 @@ int t2v_attn_bwd(const void* q, const void* k, const void* v, const void* out, c
   return t2v::guarded([&] {
     return t2v::attn_bwd_impl(q, k, v, out, lse, cu_seqlens, cu_seqlens, nseq, heads, head_dim, scale, dout, dq, dk,
                               dv, delta_ws, stream);
+  });
+}
+
+int t2v_attn_bwd_noalloc(const void* q, const void* k, const void* v, const void* out, const float* lse,
+                         const int32_t* cu_seqlens, int nseq, int heads, int head_dim, float scale, const void* dout,
+                         void* dq, void* dk, void* dv, void* stream) {
+  return t2v::guarded([&] {
+    return t2v::attn_bwd_noalloc_impl(q, k, v, out, lse, cu_seqlens, nseq, heads, head_dim, scale, dout, dq, dk, dv,
+                                      stream);
   });
 }
 

@@ -350,3 +350,18 @@ def test_attn_bwd_wrapper_rejects_before_launch(case, msg):
         lse = _cpu((H, T + 1), torch.float32)
     with pytest.raises(ValueError, match=msg):
         attn_bwd(q, k, v, out, lse, g, cu, 0.125, **kw)
+
+
+def test_noalloc_refuses_a_pack_beyond_its_scratch_before_any_device_call():
+    """t2v_attn_bwd_noalloc keeps Delta / lse (8 * heads * T bytes) and the work lists in a
+    64 MiB static array; a larger call is refused during validation (fake pointers: nothing
+    is dereferenced or launched)."""
+    L = _lib.lib()
+    H, D = 64, 64
+    T = (64 << 20) // (8 * H) + 64
+    cu = np.array([0, T], dtype=np.int32)
+    p = [A + i * 4096 * MB for i in range(9)]
+    st = L.t2v_attn_bwd_noalloc(p[0], p[1], p[2], p[3], p[4], cu.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), 1,
+                                H, D, 0.125, p[5], p[6], p[7], p[8], None)
+    msg = _lib.t2v_last_error(L)
+    assert st == INV and "bytes of scratch" in msg and "67108864" in msg, (st, msg)
