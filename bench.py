@@ -285,7 +285,7 @@ def ingest_rocpd(kt_db, fetch_db, write_db, copy_fetch_db, copy_write_db, worklo
 def mfma_cmd(out):
     """The counter pass summarised by --ingest-mfma, writing under directory `out`."""
     return (f"rocprofv3 --pmc MfmaUtil MfmaFlopsBF16 SQ_INSTS_MFMA -d {out}/pmc_mfma -o m -- "
-            "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline")
+            "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline --no-extras")
 
 
 def ingest_mfma(pmc_db, workload):
@@ -344,9 +344,9 @@ def profile_cmds(out):
     """The kernel-trace and HBM-counter passes summarised by --ingest-rocpd and
     --write-summaries, writing under directory `out`."""
     return f"""Commands (repo root, on the GPU; rocprofv3 writes rocpd SQLite files):
-  rocprofv3 --kernel-trace --stats -d {out}/prof_kt -o kt -- python3 bench.py --steps 20 --warmup 5 --no-cpu-baseline
-  rocprofv3 --pmc FETCH_SIZE -d {out}/pmc_fetch -o f -- python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline
-  rocprofv3 --pmc WRITE_SIZE -d {out}/pmc_write -o w -- python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline
+  rocprofv3 --kernel-trace --stats -d {out}/prof_kt -o kt -- python3 bench.py --steps 20 --warmup 5 --no-cpu-baseline --no-extras
+  rocprofv3 --pmc FETCH_SIZE -d {out}/pmc_fetch -o f -- python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline --no-extras
+  rocprofv3 --pmc WRITE_SIZE -d {out}/pmc_write -o w -- python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline --no-extras
   rocprofv3 --pmc FETCH_SIZE -d {out}/pmc_copy_fetch -o cf -- python3 bench.py --copy-calibration
   rocprofv3 --pmc WRITE_SIZE -d {out}/pmc_copy_write -o cw -- python3 bench.py --copy-calibration
   python3 bench.py --steps 20 --warmup 5 > {out}/bench_hetero.json
