@@ -47,7 +47,10 @@
  *
  * Environment. T2V_ORDER=natural schedules tiles in pack order instead of longest clip
  * first (for ablations); T2V_QTILE=wide or narrow forces the forward / dQ tile shape and
- * T2V_SPLIT=off disables the dK/dV loop split (ablations and tests). T2V_LOG=1 prints one
+ * T2V_SPLIT=off disables the dK/dV loop split (ablations and tests); T2V_PERSISTENT=1 runs the
+ * forward and dK/dV kernels on a persistent grid (as many workgroups as the GPU holds at once,
+ * each striding over the work list; bitwise-equal results, measured ~1% slower, so off by
+ * default). T2V_LOG=1 prints one
  * line to stderr per new work list: its items, the host's predicted list-scheduling
  * makespan and its lower bound, and the loop split if any. T2V_TEST_FAIL_ALLOC=1 makes
  * building a new work list fail with T2V_ERR_OOM, for testing that path.

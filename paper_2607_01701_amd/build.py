@@ -46,7 +46,7 @@ SCHED = {
 
 
 # Every kernel is compiled with the compiler's per-kernel resource report, and the build
-# fails if any kernel spills registers or uses scratch (private) memory. The kernels order
+# fails if any kernel spills vector registers or uses scratch (private) memory. The kernels order
 # their LDS DMA with counted `s_waitcnt vmcnt(N)` waits that assume only the DMA
 # instructions are outstanding; spill stores and reloads are vector memory operations too,
 # and would silently shift those counts (a wait would then return before its stage landed).
@@ -71,11 +71,12 @@ def kernel_resources(compiler_output: str) -> dict:
 
 
 def resource_violations(resources: dict) -> list:
-    """Kernels that spill or use scratch memory (each as a readable line)."""
+    """Kernels that spill vector registers or use scratch memory (each as a readable line).
+    SGPR spills that stay in VGPR lanes (v_writelane / v_readlane, no scratch) issue no memory
+    operations and are allowed; once they reach scratch, ScratchSize is nonzero."""
     bad = []
     for name, r in sorted(resources.items()):
-        why = [f"{k} = {r[k]}" for k in ("ScratchSize [bytes/lane]", "SGPRs Spill", "VGPRs Spill")
-               if r.get(k, "0") != "0"]
+        why = [f"{k} = {r[k]}" for k in ("ScratchSize [bytes/lane]", "VGPRs Spill") if r.get(k, "0") != "0"]
         if r.get("Dynamic Stack", "False") != "False":
             why.append("dynamic stack")
         if why:

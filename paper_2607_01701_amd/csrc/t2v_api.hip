@@ -1,6 +1,7 @@
 // C ABI of libt2vattn: argument validation, the device work-list cache, and launches.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <atomic>
 #include <cstdio>
 #include <cstdlib>
@@ -93,6 +94,15 @@ TileRule dkdv_rule(int head_dim) {
   TileRule r;
   r.wide = r.narrow = dkdv_tile_rows(head_dim);
   return r;
+}
+
+// T2V_PERSISTENT=1 launches the forward and dK/dV kernels on a persistent grid (as many
+// workgroups as the GPU holds at once, each looping over the work list with a stride of the
+// grid); the default is one workgroup per work item. Results are bitwise equal either way.
+// (The dQ kernel always runs one workgroup per item: its looping form would spill.)
+bool persistent_enabled() {
+  const char* s = std::getenv("T2V_PERSISTENT");
+  return s != nullptr && std::strcmp(s, "1") == 0;
 }
 
 // T2V_SPLIT=off disables the dK/dV loop split (for ablations).
@@ -641,6 +651,7 @@ int attn_fwd_impl(const void* q, const void* k, const void* v, const int32_t* cu
   a.total_tokens = Tq;
   a.scale = scale;
   a.trace = tracer().reserve(plan->n_items);
+  a.persistent = persistent_enabled();
   hipError_t e = timer().run(kSlotFwd, s, [&] { return launch_fwd(a, out, lse, plan->d_items, plan->n_items, s); });
   const int used = note_use(plan, s);
   if (e != hipSuccess) return hip_fail(e, "forward kernel launch");
@@ -696,6 +707,7 @@ int attn_bwd_impl(const void* q, const void* k, const void* v, const void* out, 
   a.head_dim = head_dim;
   a.total_tokens = Tq;
   a.scale = scale;
+  a.persistent = persistent_enabled();
   hipError_t e = timer().run(kSlotPre, s, [&] { return launch_bwd_pre(a, s); });
   if (e != hipSuccess) return hip_fail(e, "backward preprocess launch");
   if (pk->n_items > 0) {
@@ -825,6 +837,7 @@ int attn_bwd_noalloc_impl(const void* q, const void* k, const void* v, const voi
   a.head_dim = head_dim;
   a.total_tokens = T;
   a.scale = scale;
+  a.persistent = persistent_enabled();
   e = timer().run(kSlotPre, s, [&] { return launch_bwd_pre(a, s); });
   if (e != hipSuccess) return hip_fail(e, "backward preprocess launch");
   if (n_kv > 0) {
@@ -857,6 +870,21 @@ int guarded(F&& f) {
 }
 
 }  // namespace
+}  // namespace t2v
+
+namespace t2v {
+
+int persistent_grid(const void* kernel, int threads, int n_items) {
+  int per_cu = 0, ncu = cu_count();
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess) {
+    (void)hipGetLastError();
+    per_cu = 1;
+  }
+  int grid = std::max(1, per_cu) * std::max(1, ncu);
+  if (grid >= kNumXcd) grid -= grid % kNumXcd;
+  return std::max(1, std::min(grid, n_items));
+}
+
 }  // namespace t2v
 
 extern "C" {

@@ -133,13 +133,12 @@ T2V_DEV void dkdv_step(uint32_t qbase, uint32_t gbase, uint32_t qr0, uint32_t qr
   dkdv_grad_mfma<D>(pb, sb, qr0, qr1, gr0, gr1, qs, dka, dva);
 }
 
-template <int D>
+template <int D, bool PERSIST>
 __global__ __launch_bounds__(dkdv_threads<D>(), 1) void attn_bwd_dkdv_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
     const bf16* __restrict__ dout, const float* __restrict__ lse2, const float* __restrict__ ndelta,
     const Item* __restrict__ items, int H, int64_t T, float c, float scale, bf16* __restrict__ dk,
-    bf16* __restrict__ dv, float* __restrict__ partial, unsigned long long* __restrict__ trace) {
-  const unsigned long long trace_t0 = trace != nullptr ? trace_clock() : 0ull;
+    bf16* __restrict__ dv, float* __restrict__ partial, unsigned long long* __restrict__ trace, int n_items) {
   constexpr int KK = D / 16;
   constexpr int DB = D / 32;
   constexpr int BM = dkdv_bm<D>();  // queries per LDS stage
@@ -154,141 +153,149 @@ __global__ __launch_bounds__(dkdv_threads<D>(), 1) void attn_bwd_dkdv_kernel(
   __shared__ __attribute__((aligned(16))) float sL[NS][BM];       // lse * log2(e)
   __shared__ __attribute__((aligned(16))) float sD[NS][BM];       // -Delta
 
-  const Item it = items[blockIdx.x];
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int G = lane >> 5;
-  const int l32 = lane & 31;
-  const int Lk = it.len;   // keys of the sequence (this tile's rows)
-  const int L = it.llen;   // queries of the sequence (the loop)
-  const int64_t rs = static_cast<int64_t>(H) * D;
-  const int64_t base = static_cast<int64_t>(it.row0) * rs + static_cast<int64_t>(it.head) * D;
-  const int64_t qbase = static_cast<int64_t>(it.lrow0) * rs + static_cast<int64_t>(it.head) * D;
-  const int64_t lbase = static_cast<int64_t>(it.head) * T + it.lrow0;
-  const bf16* qh = q + qbase;
-  const bf16* gh = dout + qbase;
-  const float* vec_src = (wave < NW / 2 ? lse2 : ndelta) + lbase;
-  const int vec_off = (wave % (NW / 2)) * 32;
-  const int key_wave0 = it.tile0 + wave * 32;
-  const bool wave_active = key_wave0 < Lk;
+  // One work item per workgroup, or (persistent grid) items w, w + grid, w + 2 grid, ...: the
+  // grid is a multiple of the 8 XCDs, so every item still runs on XCD (item mod 8).
+  for (int w = blockIdx.x, first = 1; PERSIST ? w < n_items : first != 0; w += gridDim.x, first = 0) {
+    const unsigned long long trace_t0 = trace != nullptr ? trace_clock() : 0ull;
+    const Item it = items[w];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int G = lane >> 5;
+    const int l32 = lane & 31;
+    const int Lk = it.len;   // keys of the sequence (this tile's rows)
+    const int L = it.llen;   // queries of the sequence (the loop)
+    const int64_t rs = static_cast<int64_t>(H) * D;
+    const int64_t base = static_cast<int64_t>(it.row0) * rs + static_cast<int64_t>(it.head) * D;
+    const int64_t qbase = static_cast<int64_t>(it.lrow0) * rs + static_cast<int64_t>(it.head) * D;
+    const int64_t lbase = static_cast<int64_t>(it.head) * T + it.lrow0;
+    const bf16* qh = q + qbase;
+    const bf16* gh = dout + qbase;
+    const float* vec_src = (wave < NW / 2 ? lse2 : ndelta) + lbase;
+    const int vec_off = (wave % (NW / 2)) * 32;
+    const int key_wave0 = it.tile0 + wave * 32;
+    const bool wave_active = key_wave0 < Lk;
 
-  // Every wave issues exactly kOps DMA instructions per stage, so counted waits work.
-  const TileDma<D, BM, dkdv_threads<D>()> dma(tid, rs);
-  auto stage = [&](int t) {
-    const int b = t % NS, i0 = t * BM;
-    dma.copy(sQ[b], qh, rs, i0, L);
-    dma.copy(sG[b], gh, rs, i0, L);
-    float* dst = (wave < NW / 2 ? sL[b] : sD[b]) + vec_off;
-    if (lane < 32) rows64_dma(dst, vec_src, i0, vec_off, L, lane);
-  };
-  // Before reading stage t + 1: wait for it, leaving the stages issued after it in flight.
-  auto wait_next = [&](int t, int ntiles) {
-    const int after = min(NS - 2, ntiles - 2 - t);  // stages issued after t + 1
-    if (after >= NS - 2) {
-      wait_vmcnt<(NS - 2) * kOps>();
-    } else if (NS > 3 && after == 1) {
-      wait_vmcnt<kOps>();
-    } else if (NS > 4 && after == 2) {
-      wait_vmcnt<2 * kOps>();
-    } else {
-      wait_vmcnt0();
+    // Every wave issues exactly kOps DMA instructions per stage, so counted waits work.
+    const TileDma<D, BM, dkdv_threads<D>()> dma(tid, rs);
+    auto stage = [&](int t) {
+      const int b = t % NS, i0 = t * BM;
+      dma.copy(sQ[b], qh, rs, i0, L);
+      dma.copy(sG[b], gh, rs, i0, L);
+      float* dst = (wave < NW / 2 ? sL[b] : sD[b]) + vec_off;
+      if (lane < 32) rows64_dma(dst, vec_src, i0, vec_off, L, lane);
+    };
+    // Before reading stage t + 1: wait for it, leaving the stages issued after it in flight.
+    auto wait_next = [&](int t, int ntiles) {
+      const int after = min(NS - 2, ntiles - 2 - t);  // stages issued after t + 1
+      if (after >= NS - 2) {
+        wait_vmcnt<(NS - 2) * kOps>();
+      } else if (NS > 3 && after == 1) {
+        wait_vmcnt<kOps>();
+      } else if (NS > 4 && after == 2) {
+        wait_vmcnt<2 * kOps>();
+      } else {
+        wait_vmcnt0();
+      }
+    };
+    static_assert(NS >= 2 && NS <= 5, "wait_next handles up to 3 stages in flight");
+
+    const int ntiles = (L + BM - 1) / BM;
+    const int nfull = L / BM;
+    stage(0);
+
+    // K and V of this wave's 32 keys, as B operands (lane = key, elements along head dim).
+    bf16x8 kop[KK], vop[KK];
+    {
+      const int kj = key_wave0 + l32;
+      const bool ok = kj < Lk;
+  #pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        kop[kk] = load8(k + base + kj * rs + kk * 16 + G * 8, ok);
+        vop[kk] = load8(v + base + kj * rs + kk * 16 + G * 8, ok);
+      }
     }
-  };
-  static_assert(NS >= 2 && NS <= 5, "wait_next handles up to 3 stages in flight");
-
-  const int ntiles = (L + BM - 1) / BM;
-  const int nfull = L / BM;
-  stage(0);
-
-  // K and V of this wave's 32 keys, as B operands (lane = key, elements along head dim).
-  bf16x8 kop[KK], vop[KK];
-  {
-    const int kj = key_wave0 + l32;
-    const bool ok = kj < Lk;
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      kop[kk] = load8(k + base + kj * rs + kk * 16 + G * 8, ok);
-      vop[kk] = load8(v + base + kj * rs + kk * 16 + G * 8, ok);
+    f32x16 dka[DB], dva[DB];
+  #pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      dka[db] = zero16();
+      dva[db] = zero16();
     }
-  }
-  f32x16 dka[DB], dva[DB];
-#pragma unroll
-  for (int db = 0; db < DB; ++db) {
-    dka[db] = zero16();
-    dva[db] = zero16();
-  }
-  // Stage 0 and the K / V loads complete here; a wait the compiler sees also keeps it
-  // from waiting for the K / V loads inside the loop (where the stages it does not see
-  // would make that a full wait).
-  wait_vmcnt0();
-#pragma unroll
-  for (int t = 1; t < NS - 1; ++t)
-    if (t < ntiles) stage(t);
-  __syncthreads();
+    // Stage 0 and the K / V loads complete here; a wait the compiler sees also keeps it
+    // from waiting for the K / V loads inside the loop (where the stages it does not see
+    // would make that a full wait).
+    wait_vmcnt0();
+  #pragma unroll
+    for (int t = 1; t < NS - 1; ++t)
+      if (t < ntiles) stage(t);
+    __syncthreads();
 
-  const uint32_t oo = opnd_lane_off<D>(lane);
-  const uint32_t ro0 = rows_lane_off<D>(lane, 0), ro1 = rows_lane_off<D>(lane, 1);
-  for (int tt = 0; tt < nfull; ++tt) {
-    const int b = tt % NS;
-    if (tt + NS - 1 < ntiles) stage(tt + NS - 1);
-    if (wave_active) {
+    const uint32_t oo = opnd_lane_off<D>(lane);
+    const uint32_t ro0 = rows_lane_off<D>(lane, 0), ro1 = rows_lane_off<D>(lane, 1);
+    for (int tt = 0; tt < nfull; ++tt) {
+      const int b = tt % NS;
+      if (tt + NS - 1 < ntiles) stage(tt + NS - 1);
+      if (wave_active) {
+        const uint32_t tq = lds_addr(sQ[b]), tg = lds_addr(sG[b]);
+        const uint32_t qb = tq + oo, gb = tg + oo;
+        const uint32_t q0 = tq + ro0, q1 = tq + ro1, g0 = tg + ro0, g1 = tg + ro1;
+  #pragma unroll
+        for (int qs = 0; qs < BM; qs += 32)
+          dkdv_step<D, false>(qb, gb, q0, q1, g0, g1, sL[b], sD[b], qs, 32, c, kop, vop, dka, dva, lane);
+      }
+      wait_next(tt, ntiles);
+      __syncthreads();
+    }
+    if (nfull < ntiles && wave_active) {  // last tile, 1 .. BM-1 queries
+      const int b = nfull % NS;
+      const int rem = L - nfull * BM;
       const uint32_t tq = lds_addr(sQ[b]), tg = lds_addr(sG[b]);
       const uint32_t qb = tq + oo, gb = tg + oo;
       const uint32_t q0 = tq + ro0, q1 = tq + ro1, g0 = tg + ro0, g1 = tg + ro1;
-#pragma unroll
-      for (int qs = 0; qs < BM; qs += 32)
-        dkdv_step<D, false>(qb, gb, q0, q1, g0, g1, sL[b], sD[b], qs, 32, c, kop, vop, dka, dva, lane);
+  #pragma unroll
+      for (int qs = 0; qs < BM; qs += 32) {
+        if (rem >= qs + 32)
+          dkdv_step<D, false>(qb, gb, q0, q1, g0, g1, sL[b], sD[b], qs, 32, c, kop, vop, dka, dva, lane);
+        else if (rem > qs)
+          dkdv_step<D, true>(qb, gb, q0, q1, g0, g1, sL[b], sD[b], qs, rem - qs, c, kop, vop, dka, dva, lane);
+      }
     }
-    wait_next(tt, ntiles);
-    __syncthreads();
-  }
-  if (nfull < ntiles && wave_active) {  // last tile, 1 .. BM-1 queries
-    const int b = nfull % NS;
-    const int rem = L - nfull * BM;
-    const uint32_t tq = lds_addr(sQ[b]), tg = lds_addr(sG[b]);
-    const uint32_t qb = tq + oo, gb = tg + oo;
-    const uint32_t q0 = tq + ro0, q1 = tq + ro1, g0 = tg + ro0, g1 = tg + ro1;
-#pragma unroll
-    for (int qs = 0; qs < BM; qs += 32) {
-      if (rem >= qs + 32)
-        dkdv_step<D, false>(qb, gb, q0, q1, g0, g1, sL[b], sD[b], qs, 32, c, kop, vop, dka, dva, lane);
-      else if (rem > qs)
-        dkdv_step<D, true>(qb, gb, q0, q1, g0, g1, sL[b], sD[b], qs, rem - qs, c, kop, vop, dka, dva, lane);
-    }
-  }
 
-  if (wave_active && it.slot >= 0) {
-    // One piece of a split loop: unscaled fp32 sums into the item's partial slot
-    // ([dK | dV] x tile key x head dim), added up in piece order by the reduce kernel.
-    float* pk = partial + static_cast<int64_t>(it.slot) * (2 * dkdv_keys<D>() * D);
-    float* pv = pk + dkdv_keys<D>() * D;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int kr = wave * 32 + (r >> 2) * 8 + G * 4 + (r & 3);  // key within the tile
-      if (it.tile0 + kr < Lk) {
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          pk[kr * D + db * 32 + l32] = dka[db][r];
-          pv[kr * D + db * 32 + l32] = dva[db][r];
+    if (wave_active && it.slot >= 0) {
+      // One piece of a split loop: unscaled fp32 sums into the item's partial slot
+      // ([dK | dV] x tile key x head dim), added up in piece order by the reduce kernel.
+      float* pk = partial + static_cast<int64_t>(it.slot) * (2 * dkdv_keys<D>() * D);
+      float* pv = pk + dkdv_keys<D>() * D;
+  #pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int kr = wave * 32 + (r >> 2) * 8 + G * 4 + (r & 3);  // key within the tile
+        if (it.tile0 + kr < Lk) {
+  #pragma unroll
+          for (int db = 0; db < DB; ++db) {
+            pk[kr * D + db * 32 + l32] = dka[db][r];
+            pv[kr * D + db * 32 + l32] = dva[db][r];
+          }
+        }
+      }
+    } else if (wave_active) {
+      // Accumulators: lane = head-dim column db*32 + l32, register r = key 8 (r/4) + 4 G + r % 4.
+  #pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int kj = key_wave0 + (r >> 2) * 8 + G * 4 + (r & 3);
+        if (kj < Lk) {
+  #pragma unroll
+          for (int db = 0; db < DB; ++db) {
+            dk[base + kj * rs + db * 32 + l32] = static_cast<bf16>(dka[db][r] * scale);
+            dv[base + kj * rs + db * 32 + l32] = static_cast<bf16>(dva[db][r]);
+          }
         }
       }
     }
-  } else if (wave_active) {
-    // Accumulators: lane = head-dim column db*32 + l32, register r = key 8 (r/4) + 4 G + r % 4.
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int kj = key_wave0 + (r >> 2) * 8 + G * 4 + (r & 3);
-      if (kj < Lk) {
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          dk[base + kj * rs + db * 32 + l32] = static_cast<bf16>(dka[db][r] * scale);
-          dv[base + kj * rs + db * 32 + l32] = static_cast<bf16>(dva[db][r]);
-        }
-      }
+    if (trace != nullptr) trace_end(trace, trace_t0, 2, w);
+    if constexpr (PERSIST) {
+      if (w + static_cast<int>(gridDim.x) < n_items) __syncthreads();  // LDS reads done before the next item's DMA
     }
   }
-  if (trace != nullptr) trace_end(trace, trace_t0, 2);
 }
 
 // Sum of the partial slots of one split tile, in piece order, scaled (dK) and rounded to
@@ -346,9 +353,25 @@ hipError_t launch_bwd_dkdv_reduce(const AttnArgs& a, const Item* tiles, int n_ti
   return hipGetLastError();
 }
 
+namespace {
+template <int D>
+void launch_dkdv_as(const AttnArgs& a, const bf16* q, const bf16* k, const bf16* v, const bf16* g, const float* lse2,
+                    const Item* items, int n_items, float c, bf16* dk, bf16* dv, hipStream_t stream) {
+  const dim3 block(dkdv_threads<D>());
+  if (a.persistent) {
+    const void* fn = reinterpret_cast<const void*>(&attn_bwd_dkdv_kernel<D, true>);
+    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, true>), dim3(persistent_grid(fn, dkdv_threads<D>(), n_items)), block,
+                       0, stream, q, k, v, g, lse2, a.delta, items, a.heads, a.total_tokens, c, a.scale, dk, dv,
+                       a.partial, a.trace, n_items);
+  } else {
+    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, false>), dim3(n_items), block, 0, stream, q, k, v, g, lse2, a.delta,
+                       items, a.heads, a.total_tokens, c, a.scale, dk, dv, a.partial, a.trace, n_items);
+  }
+}
+}  // namespace
+
 hipError_t launch_bwd_dkdv(const AttnArgs& a, const Item* items, int n_items, hipStream_t stream) {
   const float c = a.scale * kLog2e;
-  const dim3 grid(n_items), block(a.head_dim == 64 ? dkdv_threads<64>() : dkdv_threads<128>());
   const auto* q = static_cast<const bf16*>(a.q);
   const auto* k = static_cast<const bf16*>(a.k);
   const auto* v = static_cast<const bf16*>(a.v);
@@ -357,11 +380,9 @@ hipError_t launch_bwd_dkdv(const AttnArgs& a, const Item* items, int n_items, hi
   auto* dv = static_cast<bf16*>(a.dv);
   const float* lse2 = a.delta + a.total_tokens * a.heads;
   if (a.head_dim == 128)
-    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<128>), grid, block, 0, stream, q, k, v, g, lse2, a.delta, items,
-                       a.heads, a.total_tokens, c, a.scale, dk, dv, a.partial, a.trace);
+    launch_dkdv_as<128>(a, q, k, v, g, lse2, items, n_items, c, dk, dv, stream);
   else
-    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<64>), grid, block, 0, stream, q, k, v, g, lse2, a.delta, items,
-                       a.heads, a.total_tokens, c, a.scale, dk, dv, a.partial, a.trace);
+    launch_dkdv_as<64>(a, q, k, v, g, lse2, items, n_items, c, dk, dv, stream);
   return hipGetLastError();
 }
 }  // namespace t2v

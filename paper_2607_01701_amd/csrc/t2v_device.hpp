@@ -285,15 +285,16 @@ T2V_DEV bf16x8 read_rows_opnd(uint32_t base0, uint32_t base1, int row0, int db) 
 // constant 100 MHz clock, and the kernel's slot.
 T2V_DEV unsigned long long trace_clock() { return __builtin_amdgcn_s_memrealtime(); }
 
-// Every wave of the workgroup must call this (it holds a barrier); rec is uniform.
-T2V_DEV void trace_end(unsigned long long* rec, unsigned long long t0, int slot) {
+// Every wave of the workgroup must call this (it holds a barrier); rec is uniform. `index` is the
+// work item's position in the list (the record written).
+T2V_DEV void trace_end(unsigned long long* rec, unsigned long long t0, int slot, int index) {
   __syncthreads();
   if (threadIdx.x == 0) {
     unsigned hw, xcc;
     asm volatile("s_getreg_b32 %0, hwreg(HW_REG_HW_ID)" : "=s"(hw));
     asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
     const unsigned long long t1 = __builtin_amdgcn_s_memrealtime();
-    unsigned long long* r = rec + 4 * static_cast<size_t>(blockIdx.x);
+    unsigned long long* r = rec + 4 * static_cast<size_t>(index);
     r[0] = (static_cast<unsigned long long>(xcc & 0xFu) << 16) | ((hw >> 8) & 0xFFu);
     r[1] = t0;
     r[2] = t1;

@@ -143,116 +143,123 @@ T2V_DEV void fwd_step(uint32_t kbase, uint32_t vbase0, uint32_t vbase1, int kb, 
   }
 }
 
-template <int D, int QB, bool NEG, int NT>
+template <int D, int QB, bool NEG, int NT, bool PERSIST>
 __global__ __launch_bounds__(NT, 512 / NT) void attn_fwd_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
     const Item* __restrict__ items, int H, int64_t T, float c, bf16* __restrict__ out,
-    float* __restrict__ lse, unsigned long long* __restrict__ trace) {
-  const unsigned long long trace_t0 = trace != nullptr ? trace_clock() : 0ull;
+    float* __restrict__ lse, unsigned long long* __restrict__ trace, int n_items) {
   constexpr int KK = D / 16;  // k-steps of the head-dim contraction
   constexpr int DB = D / 32;  // 32-wide head-dim blocks of the output
   constexpr int BN = kFwdBN;  // keys per LDS stage
   __shared__ __attribute__((aligned(1024))) bf16 sK[2][BN * D];
   __shared__ __attribute__((aligned(1024))) bf16 sV[2][BN * D];
 
-  const Item it = items[blockIdx.x];
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int G = lane >> 5;
-  const int l32 = lane & 31;
-  const int Lq = it.len;   // queries of the sequence (this tile's rows)
-  const int L = it.llen;   // keys of the sequence (the loop)
-  const int64_t rs = static_cast<int64_t>(H) * D;  // elements between consecutive tokens
-  const int64_t base = static_cast<int64_t>(it.row0) * rs + static_cast<int64_t>(it.head) * D;
-  const int64_t kvbase = static_cast<int64_t>(it.lrow0) * rs + static_cast<int64_t>(it.head) * D;
-  const bf16* kh = k + kvbase;
-  const bf16* vh = v + kvbase;
-  const int q_wave0 = it.tile0 + wave * QB * 32;
-  const bool wave_active = q_wave0 < Lq;
+  // One work item per workgroup, or (persistent grid) items w, w + grid, w + 2 grid, ...: the
+  // grid is a multiple of the 8 XCDs, so every item still runs on XCD (item mod 8).
+  for (int w = blockIdx.x, first = 1; PERSIST ? w < n_items : first != 0; w += gridDim.x, first = 0) {
+    const unsigned long long trace_t0 = trace != nullptr ? trace_clock() : 0ull;
+    const Item it = items[w];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int G = lane >> 5;
+    const int l32 = lane & 31;
+    const int Lq = it.len;   // queries of the sequence (this tile's rows)
+    const int L = it.llen;   // keys of the sequence (the loop)
+    const int64_t rs = static_cast<int64_t>(H) * D;  // elements between consecutive tokens
+    const int64_t base = static_cast<int64_t>(it.row0) * rs + static_cast<int64_t>(it.head) * D;
+    const int64_t kvbase = static_cast<int64_t>(it.lrow0) * rs + static_cast<int64_t>(it.head) * D;
+    const bf16* kh = k + kvbase;
+    const bf16* vh = v + kvbase;
+    const int q_wave0 = it.tile0 + wave * QB * 32;
+    const bool wave_active = q_wave0 < Lq;
 
-  const TileDma<D, BN, NT> dma(tid, rs);
-  dma.copy(sK[0], kh, rs, 0, L);
-  dma.copy(sV[0], vh, rs, 0, L);
+    const TileDma<D, BN, NT> dma(tid, rs);
+    dma.copy(sK[0], kh, rs, 0, L);
+    dma.copy(sV[0], vh, rs, 0, L);
 
-  bf16x8 qop[QB][KK];
-#pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    const int qi = q_wave0 + qb * 32 + l32;
-    const bool ok = qi < Lq;
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) qop[qb][kk] = load8(q + base + qi * rs + kk * 16 + G * 8, ok);
-  }
-
-  f32x16 o[QB][DB];
-  float m_run[QB], l_run[QB];
-#pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    m_run[qb] = -kInf;
-    l_run[qb] = 0.0f;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) o[qb][db] = zero16();
-  }
-
-  const int ntiles = (L + BN - 1) / BN;
-  const int nfull = L / BN;  // tiles with BN keys of the sequence
-  const uint32_t ko = opnd_lane_off<D>(lane);
-  const uint32_t vo0 = rows_lane_off<D>(lane, 0), vo1 = rows_lane_off<D>(lane, 1);
-  wait_vmcnt0();
-  __syncthreads();
-  for (int tt = 0; tt < nfull; ++tt) {
-    const int b = tt & 1;
-    if (tt + 1 < ntiles) {
-      dma.copy(sK[b ^ 1], kh, rs, (tt + 1) * BN, L);
-      dma.copy(sV[b ^ 1], vh, rs, (tt + 1) * BN, L);
-    }
-    if (wave_active) {
-      const uint32_t kbase = lds_addr(sK[b]) + ko;
-      const uint32_t vb0 = lds_addr(sV[b]) + vo0, vb1 = lds_addr(sV[b]) + vo1;
-#pragma unroll
-      for (int kb = 0; kb < BN; kb += 32)
-        fwd_step<D, QB, NEG, false>(kbase, vb0, vb1, kb, 32, c, qop, o, m_run, l_run, lane);
-    }
-    wait_vmcnt0();
-    __syncthreads();
-  }
-  if (nfull < ntiles && wave_active) {  // last tile, 1 .. BN-1 keys
-    const int b = nfull & 1;
-    const int rem = L - nfull * BN;
-    const uint32_t kbase = lds_addr(sK[b]) + ko;
-    const uint32_t vb0 = lds_addr(sV[b]) + vo0, vb1 = lds_addr(sV[b]) + vo1;
-#pragma unroll
-    for (int kb = 0; kb < BN; kb += 32) {
-      if (rem >= kb + 32)
-        fwd_step<D, QB, NEG, false>(kbase, vb0, vb1, kb, 32, c, qop, o, m_run, l_run, lane);
-      else if (rem > kb)
-        fwd_step<D, QB, NEG, true>(kbase, vb0, vb1, kb, rem - kb, c, qop, o, m_run, l_run, lane);
-    }
-  }
-
-  if (wave_active) {
-#pragma unroll
+    bf16x8 qop[QB][KK];
+  #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
       const int qi = q_wave0 + qb * 32 + l32;
-      const float lt = half_sum(l_run[qb]);
-      const float inv = 1.0f / lt;
-      if (qi < Lq) {
-        bf16* orow = out + base + qi * rs;
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            bf16x4 w;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) w[e] = static_cast<bf16>(o[qb][db][i * 4 + e] * inv);
-            *reinterpret_cast<bf16x4*>(orow + db * 32 + i * 8 + G * 4) = w;
-          }
-        }
-        if (G == 0) lse[static_cast<int64_t>(it.head) * T + it.row0 + qi] = (m_run[qb] + __builtin_amdgcn_logf(lt)) * kLn2;
+      const bool ok = qi < Lq;
+  #pragma unroll
+      for (int kk = 0; kk < KK; ++kk) qop[qb][kk] = load8(q + base + qi * rs + kk * 16 + G * 8, ok);
+    }
+
+    f32x16 o[QB][DB];
+    float m_run[QB], l_run[QB];
+  #pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      m_run[qb] = -kInf;
+      l_run[qb] = 0.0f;
+  #pragma unroll
+      for (int db = 0; db < DB; ++db) o[qb][db] = zero16();
+    }
+
+    const int ntiles = (L + BN - 1) / BN;
+    const int nfull = L / BN;  // tiles with BN keys of the sequence
+    const uint32_t ko = opnd_lane_off<D>(lane);
+    const uint32_t vo0 = rows_lane_off<D>(lane, 0), vo1 = rows_lane_off<D>(lane, 1);
+    wait_vmcnt0();
+    __syncthreads();
+    for (int tt = 0; tt < nfull; ++tt) {
+      const int b = tt & 1;
+      if (tt + 1 < ntiles) {
+        dma.copy(sK[b ^ 1], kh, rs, (tt + 1) * BN, L);
+        dma.copy(sV[b ^ 1], vh, rs, (tt + 1) * BN, L);
+      }
+      if (wave_active) {
+        const uint32_t kbase = lds_addr(sK[b]) + ko;
+        const uint32_t vb0 = lds_addr(sV[b]) + vo0, vb1 = lds_addr(sV[b]) + vo1;
+  #pragma unroll
+        for (int kb = 0; kb < BN; kb += 32)
+          fwd_step<D, QB, NEG, false>(kbase, vb0, vb1, kb, 32, c, qop, o, m_run, l_run, lane);
+      }
+      wait_vmcnt0();
+      __syncthreads();
+    }
+    if (nfull < ntiles && wave_active) {  // last tile, 1 .. BN-1 keys
+      const int b = nfull & 1;
+      const int rem = L - nfull * BN;
+      const uint32_t kbase = lds_addr(sK[b]) + ko;
+      const uint32_t vb0 = lds_addr(sV[b]) + vo0, vb1 = lds_addr(sV[b]) + vo1;
+  #pragma unroll
+      for (int kb = 0; kb < BN; kb += 32) {
+        if (rem >= kb + 32)
+          fwd_step<D, QB, NEG, false>(kbase, vb0, vb1, kb, 32, c, qop, o, m_run, l_run, lane);
+        else if (rem > kb)
+          fwd_step<D, QB, NEG, true>(kbase, vb0, vb1, kb, rem - kb, c, qop, o, m_run, l_run, lane);
       }
     }
+
+    if (wave_active) {
+  #pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        const int qi = q_wave0 + qb * 32 + l32;
+        const float lt = half_sum(l_run[qb]);
+        const float inv = 1.0f / lt;
+        if (qi < Lq) {
+          bf16* orow = out + base + qi * rs;
+  #pragma unroll
+          for (int db = 0; db < DB; ++db) {
+  #pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              bf16x4 w;
+  #pragma unroll
+              for (int e = 0; e < 4; ++e) w[e] = static_cast<bf16>(o[qb][db][i * 4 + e] * inv);
+              *reinterpret_cast<bf16x4*>(orow + db * 32 + i * 8 + G * 4) = w;
+            }
+          }
+          if (G == 0) lse[static_cast<int64_t>(it.head) * T + it.row0 + qi] = (m_run[qb] + __builtin_amdgcn_logf(lt)) * kLn2;
+        }
+      }
+    }
+    if (trace != nullptr) trace_end(trace, trace_t0, 0, w);
+    if constexpr (PERSIST) {
+      if (w + static_cast<int>(gridDim.x) < n_items) __syncthreads();  // LDS reads done before the next item's DMA
+    }
   }
-  if (trace != nullptr) trace_end(trace, trace_t0, 0);
 }
 
 }  // namespace
@@ -263,8 +270,14 @@ namespace {
 template <int D, bool NEG, int NT>
 void launch_fwd_as(const AttnArgs& a, const bf16* q, const bf16* k, const bf16* v, bf16* o, float* lse,
                    const Item* items, int n_items, float c, hipStream_t stream) {
-  hipLaunchKernelGGL((attn_fwd_kernel<D, kFwdQB, NEG, NT>), dim3(n_items), dim3(NT), 0, stream, q, k, v, items,
-                     a.heads, a.total_tokens, c, o, lse, a.trace);
+  if (a.persistent) {
+    const void* fn = reinterpret_cast<const void*>(&attn_fwd_kernel<D, kFwdQB, NEG, NT, true>);
+    hipLaunchKernelGGL((attn_fwd_kernel<D, kFwdQB, NEG, NT, true>), dim3(persistent_grid(fn, NT, n_items)), dim3(NT),
+                       0, stream, q, k, v, items, a.heads, a.total_tokens, c, o, lse, a.trace, n_items);
+  } else {
+    hipLaunchKernelGGL((attn_fwd_kernel<D, kFwdQB, NEG, NT, false>), dim3(n_items), dim3(NT), 0, stream, q, k, v,
+                       items, a.heads, a.total_tokens, c, o, lse, a.trace, n_items);
+  }
 }
 
 template <int D, bool NEG>

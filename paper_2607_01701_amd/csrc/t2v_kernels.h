@@ -36,7 +36,15 @@ struct AttnArgs {
   unsigned long long* trace = nullptr;
   int q_rows = 0;            // forward / dQ tile rows: selects the wide or narrow kernels
   float* partial = nullptr;  // dK/dV partial slots of split loops (work items with slot >= 0)
+  // Persistent grid: launch only as many workgroups as the GPU holds at once (a multiple of
+  // the 8 XCDs), each taking items w, w + grid, ...; otherwise one workgroup per item.
+  bool persistent = false;
 };
+
+// Workgroups of a persistent launch of `kernel` with `threads` threads: the resident
+// workgroups per CU times the CUs, rounded down to a multiple of the XCD count, at most
+// n_items (and at least 1).
+int persistent_grid(const void* kernel, int threads, int n_items);
 
 hipError_t launch_fwd(const AttnArgs& a, void* out, float* lse, const Item* items, int n_items,
                       hipStream_t stream);

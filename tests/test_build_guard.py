@@ -1,4 +1,4 @@
-"""The build refuses kernels that spill registers or use scratch memory (CPU: hipcc
+"""The build refuses kernels that spill vector registers or use scratch memory (CPU: hipcc
 cross-compiles for gfx950 here). The attention kernels order their LDS DMA with counted
 vector-memory waits, which spill traffic would silently shift; the guard keeps a future
 change from introducing it unnoticed."""
