@@ -94,6 +94,9 @@ def parse_args():
                          "of --copy-calibration) into profiles/; runs on the CPU")
     ap.add_argument("--ingest-mfma", metavar="PMC_DB",
                     help="summarise a rocprofv3 MfmaUtil / MfmaFlopsBF16 counter pass into profiles/; runs on the CPU")
+    ap.add_argument("--ingest-sq", nargs=3, metavar=("SQ_A_DB", "SQ_B_DB", "SQ_C_DB"),
+                    help="summarise three rocprofv3 SQ counter passes (wave-cycle breakdown, MFMA/VALU co-issue, LDS) "
+                         "into profiles/; runs on the CPU")
     return ap.parse_args()
 
 
@@ -340,6 +343,68 @@ def ingest_mfma(pmc_db, workload):
     print("\n".join(lines))
 
 
+SQ_PASSES = (
+    "SQ_WAVE_CYCLES SQ_BUSY_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_ANY SQ_ACTIVE_INST_ANY SQ_ACTIVE_INST_VALU "
+    "SQ_ACTIVE_INST_LDS SQ_ACTIVE_INST_MISC",
+    "SQ_VALU_MFMA_BUSY_CYCLES SQ_VALU_MFMA_COEXEC_CYCLES SQ_WAIT_INST_LDS SQ_LDS_IDX_ACTIVE SQ_LDS_BANK_CONFLICT "
+    "SQ_LDS_DATA_FIFO_FULL SQ_LDS_CMD_FIFO_FULL SQ_INST_LEVEL_LDS",
+    "SQ_INSTS_VALU SQ_INSTS_LDS SQ_INSTS_MFMA SQ_INSTS_SALU SQ_INSTS_VMEM SQ_THREAD_CYCLES_VALU SQ_ACTIVE_INST_SCA "
+    "SQ_ACTIVE_INST_VMEM",
+)
+
+
+def ingest_sq(dbs, workload):
+    """Per-kernel SQ counter summary (three passes of at most eight SQ counters each):
+    where the waves' cycles go, how often the matrix core and the VALU work at once, and how
+    busy the LDS is. Writes profiles/attn_fwd_bwd_<workload>_sq_counters.txt."""
+    import sqlite3
+
+    by = {}
+    for db in dbs:
+        c = sqlite3.connect(db)
+        rows = c.execute("select kernel_name, counter_name, count(*), avg(value) from counters_collection "
+                         "group by kernel_name, counter_name").fetchall()
+        c.close()
+        for name, cname, n, avg in rows:
+            slot = _slot(name)
+            if slot:
+                by.setdefault(slot, {})[cname] = avg
+    cmds = [f"rocprofv3 --pmc {p} -d <out>/pmc_sq{x} -o {x} -- python3 bench.py --steps 2 --warmup 1 "
+            "--no-cpu-baseline --no-extras" for p, x in zip(SQ_PASSES, "abc")]
+    lines = [f"rocprofv3 SQ counters: attention kernels, {workload} workload, averages per launch.",
+             f"Kernel source hash (bench.py kernel_source_hash): {kernel_source_hash()}", "",
+             "Commands (repo root, on the GPU):"] + ["  " + c for c in cmds] + [
+             f"  python3 bench.py --ingest-sq <out>/pmc_sqa/a_results.db <out>/pmc_sqb/b_results.db "
+             f"<out>/pmc_sqc/c_results.db --workload {workload}", ""]
+    order = ("bwd_dkdv", "bwd_dq", "fwd", "bwd_pre")
+    names = sorted({k for d in by.values() for k in d})
+    lines.append(f"{'counter':30s} " + " ".join(f"{n:>14s}" for n in order))
+    for cn in names:
+        lines.append(f"{cn:30s} " + " ".join(f"{by.get(n, {}).get(cn, float('nan')):14.4g}" for n in order))
+    lines += ["", "Ratios (per kernel):"]
+
+    def ratio(n, a, b):
+        d = by.get(n, {})
+        return d[a] / d[b] if d.get(b) else float("nan")
+
+    for label, a, b in (("waiting (any) / wave cycles", "SQ_WAIT_ANY", "SQ_WAVE_CYCLES"),
+                        ("waiting for issue / wave cycles", "SQ_WAIT_INST_ANY", "SQ_WAVE_CYCLES"),
+                        ("issuing (any) / wave cycles", "SQ_ACTIVE_INST_ANY", "SQ_WAVE_CYCLES"),
+                        ("VALU issue / wave cycles", "SQ_ACTIVE_INST_VALU", "SQ_WAVE_CYCLES"),
+                        ("LDS issue / wave cycles", "SQ_ACTIVE_INST_LDS", "SQ_WAVE_CYCLES"),
+                        ("waiting for LDS issue / wave cycles", "SQ_WAIT_INST_LDS", "SQ_WAVE_CYCLES"),
+                        ("MFMA-VALU co-execution / MFMA busy", "SQ_VALU_MFMA_COEXEC_CYCLES", "SQ_VALU_MFMA_BUSY_CYCLES"),
+                        ("LDS bank conflict / LDS active", "SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE"),
+                        ("LDS active / busy cycles", "SQ_LDS_IDX_ACTIVE", "SQ_BUSY_CYCLES"),
+                        ("LDS instructions / MFMA", "SQ_INSTS_LDS", "SQ_INSTS_MFMA"),
+                        ("VALU instructions / MFMA", "SQ_INSTS_VALU", "SQ_INSTS_MFMA")):
+        lines.append(f"  {label:38s} " + " ".join(f"{ratio(n, a, b):14.3f}" for n in order))
+    out = os.path.join(ROOT, "profiles", f"attn_fwd_bwd_{workload}_sq_counters.txt")
+    with open(out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def profile_cmds(out):
     """The kernel-trace and HBM-counter passes summarised by --ingest-rocpd and
     --write-summaries, writing under directory `out`."""
@@ -360,7 +425,7 @@ Summarised with:
 def write_summaries(bench_json, sweep_jsonl=None):
     """Text summaries under profiles/ from a bench line, profiles/hbm_traffic.json and a sweep."""
     with open(bench_json) as f:
-        b = json.loads(f.read().strip().splitlines()[-1])
+        b = json.loads([x for x in f.read().strip().splitlines() if x.startswith("{")][-1])
     with open(TRAFFIC_FILE) as f:
         t = json.load(f)
     if t["kernel_source_hash"] != b["kernel_source_hash"]:
@@ -411,7 +476,7 @@ def write_summaries(bench_json, sweep_jsonl=None):
 
     if sweep_jsonl:
         with open(sweep_jsonl) as f:
-            rows = [json.loads(x) for x in f if x.strip()]
+            rows = [json.loads(x) for x in f if x.startswith("{")]
         out = ["bench.py --sweep: every workload, fwd + bwd, one MI355X, bf16 in / fp32 accumulate, synthetic "
                "N(0,1) inputs.", f"Kernel source hash (bench.py kernel_source_hash): {rows[0]['kernel_source_hash']}",
                "", "Command (repo root, on the GPU):", f"  python3 bench.py --sweep > {sweep_jsonl}",
@@ -1199,6 +1264,9 @@ def main():
         return
     if args.ingest_mfma:
         ingest_mfma(args.ingest_mfma, workload=args.workload)
+        return
+    if args.ingest_sq:
+        ingest_sq(args.ingest_sq, workload=args.workload)
         return
     if args.write_summaries:
         write_summaries(*args.write_summaries[:2])
