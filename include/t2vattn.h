@@ -28,8 +28,10 @@
  * pointers; cu_seqlens is a HOST pointer (the tile scheduler runs on the
  * host). The library keeps only a cache of device work lists keyed by the
  * contents of cu_seqlens (released by t2v_release_cache). It holds up to 64;
- * the call that adds one more releases the least recently used, which first
- * waits for that list's device to finish its work.
+ * the call that adds one more releases the least recently used. List memory
+ * comes from pooled device and pinned chunks; a released list's memory is
+ * reused only after the launches that read it have finished (events recorded
+ * on their streams), so no call waits for the device.
  *
  * Tiles. The forward and dQ kernels own 256-query tiles (8 waves, one workgroup per CU)
  * or 128-query tiles (4 waves, two or three per CU): narrow tiles at head_dim 64, and at
