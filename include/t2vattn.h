@@ -68,6 +68,17 @@
  * last non-OK status of the calling thread. No C++ exception crosses the ABI.
  * T = 0 returns T2V_OK without launching anything; zero-length clips are
  * skipped. Calls on different streams may run concurrently.
+ *
+ * Checked library. libt2vattn_checked.so exports the same calls, built from the same
+ * sources with bounds checks, for debugging: before any kernel runs, every work list is
+ * checked on the host against cu_seqlens (each tile inside its clip, each looped-over row
+ * inside the same clip, heads and partial slots in range); on the device every row a kernel
+ * copies into LDS is checked against its clip (a failing row is not copied); and each call
+ * waits for its kernels before returning. A violation returns T2V_ERR_BOUNDS and
+ * t2v_last_error() names the work item, or the kernel, workgroup and row. Calls into it are
+ * serialised. T2V_CHECK_CANARY=n takes n rows off every bound the kernels check, so correct
+ * kernels report their clips' last rows: a way to see that the checks report. Its results
+ * equal the unchecked library's bitwise.
  */
 #ifndef T2VATTN_H
 #define T2VATTN_H
@@ -83,7 +94,9 @@ typedef enum {
   T2V_ERR_INVALID_ARG = 1, /* bad pointer, size, cu_seqlens, scale or aliasing */
   T2V_ERR_UNSUPPORTED = 2, /* head_dim other than 64 or 128 */
   T2V_ERR_HIP = 3,         /* a HIP runtime call or kernel launch failed */
-  T2V_ERR_OOM = 4          /* the work-list cache could not allocate */
+  T2V_ERR_OOM = 4,         /* the work-list cache could not allocate */
+  T2V_ERR_BOUNDS = 5       /* checked library only: a work item, or a row a kernel copies,
+                              lies outside its clip (see "Checked library" below) */
 } t2v_status;
 
 /* Tile orders for the scheduler (see t2v_build_worklist). */

@@ -6,22 +6,27 @@ status. There is no fallback: if the library is missing, calls raise.
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
+import threading
 
 import numpy as np
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libt2vattn.so")
 HOST_LIB_PATH = os.path.join(_PKG, "libt2vattn_host.so")
+# The same calls with bounds checks (debugging; see "Checked library" in include/t2vattn.h).
+CHECKED_LIB_PATH = os.path.join(_PKG, "libt2vattn_checked.so")
 
 T2V_OK = 0
 T2V_ERR_INVALID_ARG = 1
 T2V_ERR_UNSUPPORTED = 2
 T2V_ERR_HIP = 3
 T2V_ERR_OOM = 4
+T2V_ERR_BOUNDS = 5
 STATUS_NAMES = {0: "T2V_OK", 1: "T2V_ERR_INVALID_ARG", 2: "T2V_ERR_UNSUPPORTED", 3: "T2V_ERR_HIP",
-                4: "T2V_ERR_OOM"}
+                4: "T2V_ERR_OOM", 5: "T2V_ERR_BOUNDS"}
 
 ORDER_NATURAL = 0
 ORDER_LONGEST_FIRST = 1
@@ -97,16 +102,42 @@ def _declare(lib, full: bool):
 
 _lib = None
 _host_lib = None
+_checked_lib = None
+_route = threading.local()  # .checked: this thread's calls go to the checked library
 
 
 def lib():
-    """The HIP library (loaded once). Raises if it has not been built."""
+    """The HIP library (loaded once), or the checked library inside use_checked_library().
+    Raises if it has not been built."""
     global _lib
+    if getattr(_route, "checked", False):
+        return checked_lib()
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2607_01701_amd.build`")
         _lib = _declare(ctypes.CDLL(LIB_PATH), full=True)
     return _lib
+
+
+def checked_lib():
+    """The checked library (same calls, bounds-checked; loaded once). Raises if not built."""
+    global _checked_lib
+    if _checked_lib is None:
+        if not os.path.exists(CHECKED_LIB_PATH):
+            raise ImportError(f"{CHECKED_LIB_PATH} is missing: build it with `python -m paper_2607_01701_amd.build`")
+        _checked_lib = _declare(ctypes.CDLL(CHECKED_LIB_PATH), full=True)
+    return _checked_lib
+
+
+@contextlib.contextmanager
+def use_checked_library():
+    """Inside the block, this thread's calls through this module go to the checked library."""
+    prev = getattr(_route, "checked", False)
+    _route.checked = True
+    try:
+        yield checked_lib()
+    finally:
+        _route.checked = prev
 
 
 def host_lib():

@@ -3,6 +3,9 @@
 * ``libt2vattn.so``: the gfx950 kernels (hipcc) plus the host code, the product library.
 * ``libt2vattn_host.so``: the host-only scheduler/validation code (g++), loaded by CPU
   tests that must not need a GPU.
+* ``libt2vattn_checked.so``: the same sources built with ``T2V_CHECKED=1``, a debugging
+  variant whose calls validate every work list on the host, check every row the kernels copy
+  into LDS on the device, and wait for their kernels (T2V_ERR_BOUNDS on a violation).
 
 Run ``python -m paper_2607_01701_amd.build`` (or ``__graft_entry__.build()``).
 """
@@ -21,6 +24,8 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libt2vattn.so")
 HOST_LIB = os.path.join(PKG, "libt2vattn_host.so")
+CHECKED_LIB = os.path.join(PKG, "libt2vattn_checked.so")
+CHECKED_FLAGS = ["-DT2V_CHECKED=1"]
 
 HIP_SOURCES = ["t2v_fwd.hip", "t2v_bwd_pre.hip", "t2v_bwd_dkdv.hip", "t2v_bwd_dq.hip", "t2v_api.hip",
                "t2v_probe.hip"]
@@ -47,9 +52,11 @@ SCHED = {
 
 # Every kernel is compiled with the compiler's per-kernel resource report, and the build
 # fails if any kernel spills vector registers or uses scratch (private) memory. The kernels order
-# their LDS DMA with counted `s_waitcnt vmcnt(N)` waits that assume only the DMA
-# instructions are outstanding; spill stores and reloads are vector memory operations too,
-# and would silently shift those counts (a wait would then return before its stage landed).
+# their LDS DMA with counted `s_waitcnt vmcnt(N)` waits that count only the DMA instructions;
+# spill stores and reloads are vector memory operations too. Operations complete in issue
+# order, so extra ones only make such a wait stricter (slower), never early; but the kernels'
+# register and LDS budgets, their wait depths and their measured speed all assume none, so a
+# change that starts spilling is stopped here, on the CPU, before it reaches a GPU.
 RESOURCE_REMARKS = ["-Rpass-analysis=kernel-resource-usage"]
 _REMARK = re.compile(r"remark:\s+(Function Name|ScratchSize \[bytes/lane\]|SGPRs Spill|VGPRs Spill|"
                      r"Dynamic Stack|VGPRs|AGPRs):\s+(\S+)")
@@ -96,31 +103,37 @@ def _run(cmd, verbose, check_resources=False):
         res = kernel_resources(r.stdout)
         bad = resource_violations(res)
         if bad:
-            raise RuntimeError("kernels spill registers or use scratch memory (not allowed: the counted LDS-DMA "
-                               "waits assume no other vector memory traffic):\n  " + "\n  ".join(bad))
+            raise RuntimeError("kernels spill registers or use scratch memory (not allowed: the kernels' "
+                               "counted LDS-DMA waits and register budgets assume none):\n  " + "\n  ".join(bad))
     if verbose and out.strip():
         print(out, flush=True)
 
 
 def build(verbose: bool = True) -> None:
-    os.makedirs(BUILD, exist_ok=True)
+    checked_dir = os.path.join(BUILD, "checked")
+    os.makedirs(checked_dir, exist_ok=True)
     jobs = []
-    objs = []
+    objs, checked_objs, host_objs = [], [], []
     for s in HIP_SOURCES:
         o = os.path.join(BUILD, s + ".o")
         objs.append(o)
         jobs.append(([HIPCC, *HIP_FLAGS, *SCHED.get(s, []), *RESOURCE_REMARKS, "-c", os.path.join(CSRC, s), "-o", o],
                      True))
+        o = os.path.join(checked_dir, s + ".o")
+        checked_objs.append(o)
+        jobs.append(([HIPCC, *HIP_FLAGS, *CHECKED_FLAGS, *SCHED.get(s, []), *RESOURCE_REMARKS, "-c",
+                      os.path.join(CSRC, s), "-o", o], True))
     for s in HOST_SOURCES:
         o = os.path.join(BUILD, s + ".o")
-        objs.append(o)
+        host_objs.append(o)
         jobs.append(([CXX, *COMMON, "-c", os.path.join(CSRC, s), "-o", o], False))
     with cf.ThreadPoolExecutor(max_workers=6) as ex:
         for f in [ex.submit(_run, j, verbose, chk) for j, chk in jobs]:
             f.result()
-    tmp = LIB + ".tmp"
-    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp], verbose)
-    os.replace(tmp, LIB)
+    for lib, hip_objs in ((LIB, objs), (CHECKED_LIB, checked_objs)):
+        tmp = lib + ".tmp"
+        _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *hip_objs, *host_objs, "-o", tmp], verbose)
+        os.replace(tmp, lib)
     tmp = HOST_LIB + ".tmp"
     _run([CXX, *COMMON, "-shared", *(os.path.join(CSRC, s) for s in HOST_SOURCES), "-o", tmp], verbose)
     os.replace(tmp, HOST_LIB)

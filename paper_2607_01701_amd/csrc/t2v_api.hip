@@ -334,6 +334,9 @@ struct Plan {
   ListPool::Block mem;             // d_items' block in the device pool
   hipEvent_t ready = nullptr;      // upload finished (from the device pool's event pool)
   std::vector<std::pair<hipStream_t, hipEvent_t>> uses;  // last launch reading d_items, per stream
+#if T2V_CHECKED
+  std::vector<Item> host_items;  // checked builds: the list as uploaded, validated at every call
+#endif
   ~Plan() {
     DevicePools& p = pools(device);
     std::lock_guard<std::mutex> lock(p.mu);
@@ -430,6 +433,9 @@ class PlanCache {
       items.insert(items.end(), red.begin(), red.end());
     }
     const size_t bytes = items.size() * sizeof(Item);
+#if T2V_CHECKED
+    p->host_items = items;
+#endif
     if (log_enabled()) {
       double ms = 0.0, lb = 0.0;
       plan_makespan(items.data(), p->n_items, block, ncu > 0 ? ncu : 1, &ms, &lb);
@@ -498,6 +504,80 @@ PlanCache& cache() {
   static PlanCache* c = new PlanCache();  // never destroyed: no HIP calls at process exit
   return *c;
 }
+
+#if T2V_CHECKED
+// ---------------------------------------------------------------- checked library
+//
+// Built from the same sources with T2V_CHECKED=1: before any kernel runs, every work list is
+// validated on the host against the call's offsets (check_work_items: tile rows against
+// cu_seqlens, heads, loop pieces, partial slots); after the launches the call waits for its
+// kernels and reads back their device-side DMA row checks. Calls are serialised, since the
+// device records belong to the kernel source files, not to calls. A violation returns
+// T2V_ERR_BOUNDS naming the list item, or the kernel, workgroup, row and segment length.
+std::mutex& checked_mu() {
+  static std::mutex m;
+  return m;
+}
+
+// T2V_CHECK_CANARY=n takes n rows off every bound the kernels check (a correct kernel then
+// reports its segments' last rows), to show that the device-side checks report.
+unsigned int check_canary() {
+  const char* e = std::getenv("T2V_CHECK_CANARY");
+  return e != nullptr ? static_cast<unsigned int>(std::max(0, std::atoi(e))) : 0u;
+}
+
+int check_list(const std::vector<Item>& items, int n_items, int n_reduce, const int32_t* cu_own,
+               const int32_t* cu_loop, int nseq, int heads, int block, int64_t max_slots, const char* kernel) {
+  std::string why = check_work_items(items.data(), n_items, cu_own, cu_loop, nseq, heads, block, max_slots, false);
+  if (why.empty() && n_reduce > 0)
+    why = check_work_items(items.data() + n_items, n_reduce, cu_own, cu_loop, nseq, heads, block, max_slots, true);
+  if (!why.empty()) return set_error(T2V_ERR_BOUNDS, std::string("checked library: ") + kernel + " work list, " + why);
+  return T2V_OK;
+}
+
+int check_plan(const PlanRef& p, const int32_t* cu_own, const int32_t* cu_loop, int nseq, int heads,
+               int64_t max_slots, const char* kernel) {
+  return check_list(p->host_items, p->n_items, p->n_reduce, cu_own, cu_loop, nseq, heads, p->block, max_slots,
+                    kernel);
+}
+
+// Set by check_arm once a call is about to launch kernels: only such calls wait for the device
+// afterwards (a call refused by validation, or with nothing to do, makes no device call).
+thread_local bool t_check_armed = false;
+
+// Clears the kernels' DMA row records and sets the canary, just before a call's first launch.
+int check_arm() {
+  const unsigned int canary = check_canary();
+  unsigned int rec[4];
+  for (auto take : {fwd_check_take, dkdv_check_take, dq_check_take}) {
+    const hipError_t e = take(rec, canary);
+    if (e != hipSuccess) return hip_fail(e, "clearing the DMA row checks");
+  }
+  t_check_armed = true;
+  return T2V_OK;
+}
+
+// Waits for this call's kernels, then reports the first DMA row found outside its segment.
+int check_collect(hipStream_t s) {
+  hipError_t e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "waiting for the checked kernels");
+  const char* names[3] = {"forward", "dK/dV", "dQ"};
+  hipError_t (*takes[3])(unsigned int*, unsigned int) = {fwd_check_take, dkdv_check_take, dq_check_take};
+  int status = T2V_OK;
+  for (int i = 0; i < 3; ++i) {
+    unsigned int rec[4];
+    e = takes[i](rec, 0u);
+    if (e != hipSuccess) return hip_fail(e, "reading the DMA row checks");
+    if (rec[0] != 0u && status == T2V_OK)
+      status = set_error(T2V_ERR_BOUNDS, std::string("checked library: ") + names[i] + " kernel, workgroup " +
+                                             std::to_string(rec[1]) + " copied row " +
+                                             std::to_string(static_cast<int>(rec[2])) + " of a " +
+                                             std::to_string(rec[3]) + "-row segment (" + std::to_string(rec[0]) +
+                                             " rows outside their segments in this call)");
+  }
+  return status;
+}
+#endif
 
 int64_t tensor_bytes(int64_t T, int heads, int head_dim) { return T * heads * head_dim * 2; }
 
@@ -640,7 +720,13 @@ int attn_fwd_impl(const void* q, const void* k, const void* v, const int32_t* cu
   hipStream_t s = static_cast<hipStream_t>(stream);
   PlanRef plan;
   if (int st = cache().get(cu_q, cu_k, nseq, heads, fwd_rule(head_dim), order_from_env(), 0, s, &plan)) return st;
+#if T2V_CHECKED
+  if (int st = check_plan(plan, cu_q, cu_k, nseq, heads, 0, "forward")) return st;
+#endif
   if (plan->n_items == 0) return T2V_OK;
+#if T2V_CHECKED
+  if (int st = check_arm()) return st;
+#endif
   AttnArgs a{};
   a.q_rows = plan->block;
   a.q = q;
@@ -690,6 +776,10 @@ int attn_bwd_impl(const void* q, const void* k, const void* v, const void* out, 
                 .chunk;
   if (int st = cache().get(cu_k, cu_q, nseq, heads, dkdv_rule(head_dim), order, chunk, s, &pk)) return st;
   if (int st = cache().get(cu_q, cu_k, nseq, heads, dq_rule(head_dim), order, 0, s, &pq)) return st;
+#if T2V_CHECKED
+  if (int st = check_plan(pk, cu_k, cu_q, nseq, heads, qb / dkdv_partial_slot_bytes(head_dim), "dK/dV")) return st;
+  if (int st = check_plan(pq, cu_q, cu_k, nseq, heads, 0, "dQ")) return st;
+#endif
   AttnArgs a{};
   a.q_rows = pq->block;
   a.partial = static_cast<float*>(dq);
@@ -708,6 +798,9 @@ int attn_bwd_impl(const void* q, const void* k, const void* v, const void* out, 
   a.total_tokens = Tq;
   a.scale = scale;
   a.persistent = persistent_enabled();
+#if T2V_CHECKED
+  if (int st = check_arm()) return st;
+#endif
   hipError_t e = timer().run(kSlotPre, s, [&] { return launch_bwd_pre(a, s); });
   if (e != hipSuccess) return hip_fail(e, "backward preprocess launch");
   if (pk->n_items > 0) {
@@ -805,6 +898,12 @@ int attn_bwd_noalloc_impl(const void* q, const void* k, const void* v, const voi
                                       : choose_tile_rows(cu, cu, nseq, heads, qr.wide, qr.narrow, qr.narrow_always,
                                                          qr.max_loop, qr.penalty, order, ncu, &ql);
   if (ql.empty()) ql = build_worklist(cu, cu, nseq, heads, q_rows, order);
+#if T2V_CHECKED
+  if (int st = check_list(kv, n_kv, n_reduce, cu, cu, nseq, heads, kv_rows, tb / dkdv_partial_slot_bytes(head_dim),
+                          "dK/dV"))
+    return st;
+  if (int st = check_list(ql, static_cast<int>(ql.size()), 0, cu, cu, nseq, heads, q_rows, 0, "dQ")) return st;
+#endif
   const size_t kv_bytes = align_up(kv.size() * sizeof(Item)), q_bytes = align_up(ql.size() * sizeof(Item));
   if (delta_bytes + kv_bytes + q_bytes > kNoAllocScratchBytes) return too_big(delta_bytes + kv_bytes + q_bytes);
   int device = 0;
@@ -838,6 +937,9 @@ int attn_bwd_noalloc_impl(const void* q, const void* k, const void* v, const voi
   a.total_tokens = T;
   a.scale = scale;
   a.persistent = persistent_enabled();
+#if T2V_CHECKED
+  if (int st = check_arm()) return st;
+#endif
   e = timer().run(kSlotPre, s, [&] { return launch_bwd_pre(a, s); });
   if (e != hipSuccess) return hip_fail(e, "backward preprocess launch");
   if (n_kv > 0) {
@@ -869,6 +971,23 @@ int guarded(F&& f) {
   }
 }
 
+// Runs an attention call; in the checked library, serialised and followed by the kernels'
+// device-side checks.
+template <typename F>
+int checked_call(void* stream, F&& f) {
+#if T2V_CHECKED
+  std::lock_guard<std::mutex> lock(checked_mu());
+  t_check_armed = false;
+  const int st = f();
+  if (st != T2V_OK || !t_check_armed) return st;
+  t_check_armed = false;
+  return check_collect(static_cast<hipStream_t>(stream));
+#else
+  (void)stream;
+  return f();
+#endif
+}
+
 }  // namespace
 }  // namespace t2v
 
@@ -892,7 +1011,9 @@ extern "C" {
 int t2v_attn_fwd(const void* q, const void* k, const void* v, const int32_t* cu_seqlens, int nseq, int heads,
                  int head_dim, float scale, void* out, float* lse, void* stream) {
   return t2v::guarded([&] {
-    return t2v::attn_fwd_impl(q, k, v, cu_seqlens, cu_seqlens, nseq, heads, head_dim, scale, out, lse, stream);
+    return t2v::checked_call(stream, [&] {
+      return t2v::attn_fwd_impl(q, k, v, cu_seqlens, cu_seqlens, nseq, heads, head_dim, scale, out, lse, stream);
+    });
   });
 }
 
@@ -900,8 +1021,10 @@ int t2v_attn_bwd(const void* q, const void* k, const void* v, const void* out, c
                  const int32_t* cu_seqlens, int nseq, int heads, int head_dim, float scale, const void* dout,
                  void* dq, void* dk, void* dv, float* delta_ws, void* stream) {
   return t2v::guarded([&] {
-    return t2v::attn_bwd_impl(q, k, v, out, lse, cu_seqlens, cu_seqlens, nseq, heads, head_dim, scale, dout, dq, dk,
-                              dv, delta_ws, stream);
+    return t2v::checked_call(stream, [&] {
+      return t2v::attn_bwd_impl(q, k, v, out, lse, cu_seqlens, cu_seqlens, nseq, heads, head_dim, scale, dout, dq,
+                                dk, dv, delta_ws, stream);
+    });
   });
 }
 
@@ -909,8 +1032,10 @@ int t2v_attn_bwd_noalloc(const void* q, const void* k, const void* v, const void
                          const int32_t* cu_seqlens, int nseq, int heads, int head_dim, float scale, const void* dout,
                          void* dq, void* dk, void* dv, void* stream) {
   return t2v::guarded([&] {
-    return t2v::attn_bwd_noalloc_impl(q, k, v, out, lse, cu_seqlens, nseq, heads, head_dim, scale, dout, dq, dk, dv,
-                                      stream);
+    return t2v::checked_call(stream, [&] {
+      return t2v::attn_bwd_noalloc_impl(q, k, v, out, lse, cu_seqlens, nseq, heads, head_dim, scale, dout, dq, dk,
+                                        dv, stream);
+    });
   });
 }
 
@@ -920,7 +1045,9 @@ int t2v_attn_fwd_qk(const void* q, const void* k, const void* v, const int32_t* 
   return t2v::guarded([&] {
     if (cu_seqlens_q == nullptr || cu_seqlens_k == nullptr)
       return t2v::set_error(T2V_ERR_INVALID_ARG, "cu_seqlens_q or cu_seqlens_k is NULL");
-    return t2v::attn_fwd_impl(q, k, v, cu_seqlens_q, cu_seqlens_k, nseq, heads, head_dim, scale, out, lse, stream);
+    return t2v::checked_call(stream, [&] {
+      return t2v::attn_fwd_impl(q, k, v, cu_seqlens_q, cu_seqlens_k, nseq, heads, head_dim, scale, out, lse, stream);
+    });
   });
 }
 
@@ -930,8 +1057,10 @@ int t2v_attn_bwd_qk(const void* q, const void* k, const void* v, const void* out
   return t2v::guarded([&] {
     if (cu_seqlens_q == nullptr || cu_seqlens_k == nullptr)
       return t2v::set_error(T2V_ERR_INVALID_ARG, "cu_seqlens_q or cu_seqlens_k is NULL");
-    return t2v::attn_bwd_impl(q, k, v, out, lse, cu_seqlens_q, cu_seqlens_k, nseq, heads, head_dim, scale, dout, dq,
-                              dk, dv, delta_ws, stream);
+    return t2v::checked_call(stream, [&] {
+      return t2v::attn_bwd_impl(q, k, v, out, lse, cu_seqlens_q, cu_seqlens_k, nseq, heads, head_dim, scale, dout,
+                                dq, dk, dv, delta_ws, stream);
+    });
   });
 }
 

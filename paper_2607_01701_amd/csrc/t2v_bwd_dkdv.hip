@@ -28,6 +28,12 @@ constexpr int dkdv_keys() { return dkdv_threads<D>() / 64 * 32; }
 // relative to i0 and the offset stays in [0, L - 1 - i0].
 T2V_DEV void rows64_dma(float* lds, const float* g, int i0, int off, int L, int lane) {
   const uint32_t r = static_cast<uint32_t>(min(off + lane, L - 1 - i0));
+#if T2V_CHECKED
+  if (!check_row(i0 + static_cast<int>(r), L)) {  // copy the segment's first row instead
+    dma_lds4_s(g, 0u, static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void*)lds)));
+    return;
+  }
+#endif
   dma_lds4_s(g + i0, r * 4, static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void*)lds)));
 }
 
@@ -385,4 +391,7 @@ hipError_t launch_bwd_dkdv(const AttnArgs& a, const Item* items, int n_items, hi
     launch_dkdv_as<64>(a, q, k, v, g, lse2, items, n_items, c, dk, dv, stream);
   return hipGetLastError();
 }
+#if T2V_CHECKED
+hipError_t dkdv_check_take(unsigned int* rec, unsigned int canary) { return kern::check_take_here(rec, canary); }
+#endif
 }  // namespace t2v

@@ -238,4 +238,7 @@ hipError_t launch_bwd_dq(const AttnArgs& a, const Item* items, int n_items, hipS
   }
   return hipGetLastError();
 }
+#if T2V_CHECKED
+hipError_t dq_check_take(unsigned int* rec, unsigned int canary) { return kern::check_take_here(rec, canary); }
+#endif
 }  // namespace t2v

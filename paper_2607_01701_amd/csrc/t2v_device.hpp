@@ -140,6 +140,35 @@ T2V_DEV void dma_lds4_s(const void* sbase, uint32_t voff, uint32_t lds) {
                : "memory");
 }
 
+// ---------------------------------------------------------------------- checked builds
+//
+// Compiled with T2V_CHECKED=1 (the separate checked library), every DMA checks that the row
+// it copies lies inside its segment (the clip, or the piece of it a work item loops over).
+// Each kernel source file keeps one record per device, {violations, workgroup, row, bound,
+// canary}; the host clears it before a call and reads it after the call's kernels finish.
+// The canary (set by the host on request) shortens every bound by that many rows, so correct
+// kernels report their segments' last rows; the copies themselves are unchanged. A row that
+// fails the check is not copied: the DMA reads the segment's first row instead, keeping every
+// wave's count of DMA instructions (and so the counted waits) as in the unchecked kernels.
+#ifndef T2V_CHECKED
+#define T2V_CHECKED 0
+#endif
+#if T2V_CHECKED
+static __device__ unsigned int t2v_check_rec[5];
+
+// True when 0 <= row < bound - canary; otherwise counts a violation and keeps the first.
+T2V_DEV bool check_row(int row, int bound) {
+  const int b = bound - static_cast<int>(t2v_check_rec[4]);
+  if (row >= 0 && row < b) return true;
+  if (atomicAdd(&t2v_check_rec[0], 1u) == 0u) {
+    t2v_check_rec[1] = blockIdx.x;
+    t2v_check_rec[2] = static_cast<unsigned int>(row);
+    t2v_check_rec[3] = static_cast<unsigned int>(bound);
+  }
+  return false;
+}
+#endif
+
 // Asynchronous copy of rows row0 .. row0 + R - 1 of one (clip, head) into a swizzled LDS
 // tile with global_load_lds_dwordx4 (each wave instruction fills 1 KB of LDS; lane i the
 // 16 bytes at offset 16 i). Rows at or past `L` are replaced by row L - 1, so the tile only
@@ -180,12 +209,26 @@ struct TileDma {
     const int64_t step = static_cast<int64_t>(RPI * NW) * rs * 2;  // bytes between instructions
     if (row0 + R <= L) {
 #pragma unroll
-      for (int j = 0; j < NJ; ++j) dma_lds16_s(base + j * step, off0, lds0 + j * NW * 1024);
+      for (int j = 0; j < NJ; ++j) {
+#if T2V_CHECKED
+        if (!check_row(row0 + r0 + RPI * NW * j, L)) {
+          dma_lds16_s(g, col, lds0 + j * NW * 1024);
+          continue;
+        }
+#endif
+        dma_lds16_s(base + j * step, off0, lds0 + j * NW * 1024);
+      }
     } else {
       const int last = L - 1 - row0;
 #pragma unroll
       for (int j = 0; j < NJ; ++j) {
         const int r = min(r0 + RPI * NW * j, last);
+#if T2V_CHECKED
+        if (!check_row(row0 + r, L)) {
+          dma_lds16_s(g, col, lds0 + j * NW * 1024);
+          continue;
+        }
+#endif
         dma_lds16_s(base, static_cast<uint32_t>(r) * static_cast<uint32_t>(rs * 2) + col, lds0 + j * NW * 1024);
       }
     }

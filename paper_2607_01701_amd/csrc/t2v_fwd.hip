@@ -313,4 +313,7 @@ hipError_t launch_fwd(const AttnArgs& a, void* out, float* lse, const Item* item
   }
   return hipGetLastError();
 }
+#if T2V_CHECKED
+hipError_t fwd_check_take(unsigned int* rec, unsigned int canary) { return kern::check_take_here(rec, canary); }
+#endif
 }  // namespace t2v

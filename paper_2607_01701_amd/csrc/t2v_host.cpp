@@ -217,6 +217,41 @@ std::vector<Item> build_reduce_list(const int32_t* cu, const int32_t* cul, int n
   return out;
 }
 
+std::string check_work_items(const Item* items, int n, const int32_t* cu_own, const int32_t* cu_loop, int nseq,
+                             int heads, int block, int64_t max_slots, bool reduce) {
+  for (int i = 0; i < n; ++i) {
+    const Item& it = items[i];
+    auto bad = [&](const char* what) {
+      return "item " + std::to_string(i) + " {row0 " + std::to_string(it.row0) + ", len " + std::to_string(it.len) +
+             ", tile0 " + std::to_string(it.tile0) + ", head " + std::to_string(it.head) + ", lrow0 " +
+             std::to_string(it.lrow0) + ", llen " + std::to_string(it.llen) + ", slot " + std::to_string(it.slot) +
+             ", pieces " + std::to_string(it.pieces) + "}: " + what;
+    };
+    // The segment starting at row0: the last s with cu_own[s] <= row0 (empty clips before a
+    // non-empty one share its start, so this is the non-empty one when there is one).
+    const int s = static_cast<int>(std::upper_bound(cu_own, cu_own + nseq + 1, it.row0) - cu_own) - 1;
+    if (s < 0 || s >= nseq || cu_own[s] != it.row0) return bad("row0 is not the start of a clip");
+    if (it.len < 1 || it.len != cu_own[s + 1] - cu_own[s]) return bad("len is not its clip's length");
+    if (it.tile0 < 0 || it.tile0 >= it.len || it.tile0 % block != 0) return bad("tile0 is outside the clip");
+    if (it.head < 0 || it.head >= heads) return bad("head is out of range");
+    if (reduce) {
+      if (it.slot < 0 || it.pieces < 2 || static_cast<int64_t>(it.slot) + it.pieces > max_slots)
+        return bad("partial slots are out of range");
+      continue;
+    }
+    const int32_t a = cu_loop[s], b = cu_loop[s + 1];
+    if (it.llen < 1 || it.lrow0 < a || static_cast<int64_t>(it.lrow0) + it.llen > b)
+      return bad("looped-over rows leave the clip's segment");
+    if (it.slot < 0) {
+      if (it.slot != -1 || it.pieces != 1 || it.lrow0 != a || it.llen != b - a)
+        return bad("an unsplit item must loop over its whole segment");
+    } else if (it.pieces < 2 || it.slot >= max_slots) {
+      return bad("partial slot is out of range");
+    }
+  }
+  return std::string();
+}
+
 std::vector<Item> build_worklist(const int32_t* cu, const int32_t* cu_loop, int nseq, int heads, int block,
                                  int order, int chunk) {
   std::vector<Group> groups = make_groups(cu, cu_loop, nseq, heads, block, chunk);

@@ -97,6 +97,17 @@ int choose_tile_rows(const int32_t* cu_own, const int32_t* cu_loop, int nseq, in
 std::vector<Item> build_reduce_list(const int32_t* cu_own, const int32_t* cu_loop, int nseq, int heads, int block,
                                     int chunk);
 
+// Checks a kernel work list against the offsets it was built from (tile rows against
+// cu_seqlens): each item's owned rows are one whole non-empty segment s of cu_own, its tile
+// starts inside that segment at a multiple of `block`, its head is in [0, heads), and its
+// looped-over rows lie inside segment s of cu_loop: all of it (slot = -1, pieces = 1), or one
+// piece of it writing partial slot `slot` < max_slots (pieces >= 2). Items of a reduce list
+// (reduce = true) have no loop; they need slots [slot, slot + pieces) below max_slots, with
+// pieces >= 2. Returns an empty string for a valid list, else what is wrong with the first
+// bad item. (Used by the checked library before a list reaches the GPU.)
+std::string check_work_items(const Item* items, int n, const int32_t* cu_own, const int32_t* cu_loop, int nseq,
+                             int heads, int block, int64_t max_slots, bool reduce);
+
 // First-fit allocator of byte ranges inside one memory chunk of `size` bytes (host-side
 // bookkeeping only: the chunk itself is device or pinned host memory owned by the caller).
 // Sizes are rounded up to kAlign; freed neighbours coalesce.

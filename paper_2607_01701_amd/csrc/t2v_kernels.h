@@ -53,4 +53,13 @@ hipError_t launch_bwd_dkdv(const AttnArgs& a, const Item* items, int n_items, hi
 hipError_t launch_bwd_dkdv_reduce(const AttnArgs& a, const Item* tiles, int n_tiles, hipStream_t stream);
 hipError_t launch_bwd_dq(const AttnArgs& a, const Item* items, int n_items, hipStream_t stream);
 
+#if T2V_CHECKED
+// Checked builds only: the DMA row record of the forward, dK/dV and dQ kernel sources
+// ({violations, first violating workgroup, its row, the segment length}); each call clears
+// the record and sets the canary (rows taken off every bound) for the next launches.
+hipError_t fwd_check_take(unsigned int* rec, unsigned int canary);
+hipError_t dkdv_check_take(unsigned int* rec, unsigned int canary);
+hipError_t dq_check_take(unsigned int* rec, unsigned int canary);
+#endif
+
 }  // namespace t2v

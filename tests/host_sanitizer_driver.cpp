@@ -1,5 +1,6 @@
 // Randomised exercise of the host-side code of libt2vattn (tile scheduler and its loop
-// split, makespan model, argument validation, cascade planner, work-list pool allocator), built with AddressSanitizer and
+// split, makespan model, argument validation, cascade planner, work-list pool allocator, the
+// checked library's work-list checks), built with AddressSanitizer and
 // UndefinedBehaviorSanitizer by tests/test_host_sanitizers.py. Every check that fails prints
 // a line; the exit status is the number of failed checks (sanitizer reports abort earlier).
 #include <algorithm>
@@ -325,8 +326,83 @@ static void range_allocator(std::mt19937& rng) {
   }
 }
 
+// Work-list checks of the checked library: lists the scheduler builds pass (self and cross
+// offsets, with and without the loop split); one corrupted field of one item is reported.
+static void work_item_checks(std::mt19937& rng) {
+  int corrupted = 0;
+  for (int rep = 0; rep < 150; ++rep) {
+    const int nseq = std::uniform_int_distribution<int>(1, 10)(rng);
+    const int heads = std::uniform_int_distribution<int>(1, 4)(rng);
+    const int block = 128;
+    const std::vector<int32_t> own = random_cu(rng, nseq, 700);
+    std::vector<int32_t> loop = own;
+    if (rep % 2) {  // cross offsets: every sequence with rows gets at least one looped-over row
+      loop = random_cu(rng, nseq, 9000);
+      for (int s = 0, add = 0; s < nseq; ++s) {
+        if (own[s + 1] > own[s] && loop[s + 1] + add == loop[s]) ++add;
+        loop[s + 1] += add;
+      }
+    }
+    const int chunk = rep % 3 == 0 ? 2048 : 0;
+    std::vector<t2v::Item> items =
+        t2v::build_worklist(own.data(), loop.data(), nseq, heads, block, T2V_ORDER_LONGEST_FIRST, chunk);
+    std::vector<t2v::Item> red = t2v::build_reduce_list(own.data(), loop.data(), nseq, heads, block, chunk);
+    int64_t slots = 0;
+    for (const auto& r : red) slots += r.pieces;
+    const int n = static_cast<int>(items.size());
+    CHECK(t2v::check_work_items(items.data(), n, own.data(), loop.data(), nseq, heads, block, slots, false).empty(),
+          "a scheduler list passes");
+    CHECK(t2v::check_work_items(red.data(), static_cast<int>(red.size()), own.data(), loop.data(), nseq, heads,
+                                block, slots, true).empty(), "a reduce list passes");
+    if (n == 0) continue;
+    const int i = std::uniform_int_distribution<int>(0, n - 1)(rng);
+    const t2v::Item good = items[i];
+    const bool split = good.slot >= 0;
+    int s = 0;  // the item's clip (the last with this start: earlier empty clips share it)
+    for (int j = 0; j < nseq; ++j)
+      if (own[j] == good.row0 && own[j + 1] > own[j]) s = j;
+    const int32_t before = loop[s] - 1, past = loop[s + 1] - good.lrow0 + 1;  // one row outside the segment
+    const std::vector<std::pair<const char*, t2v::Item>> bad = {
+        {"row0 is not the start", {good.row0 + 1, good.len, good.tile0, good.head, good.lrow0, good.llen, good.slot,
+                                   good.pieces}},
+        {"len is not", {good.row0, good.len + 1, good.tile0, good.head, good.lrow0, good.llen, good.slot, good.pieces}},
+        {"tile0 is outside", {good.row0, good.len, good.len + (block - good.len % block) % block, good.head,
+                              good.lrow0, good.llen, good.slot, good.pieces}},
+        {"tile0 is outside", {good.row0, good.len, good.tile0 + 1, good.head, good.lrow0, good.llen, good.slot,
+                              good.pieces}},
+        {"head is out of range", {good.row0, good.len, good.tile0, heads, good.lrow0, good.llen, good.slot,
+                                  good.pieces}},
+        {"head is out of range", {good.row0, good.len, good.tile0, -1, good.lrow0, good.llen, good.slot, good.pieces}},
+        {"looped-over rows leave", {good.row0, good.len, good.tile0, good.head, before, good.llen, good.slot,
+                                    good.pieces}},
+        {"looped-over rows leave", {good.row0, good.len, good.tile0, good.head, good.lrow0, past, good.slot,
+                                    good.pieces}},
+        {split ? "partial slot is out of range" : "an unsplit item",
+         {good.row0, good.len, good.tile0, good.head, good.lrow0, good.llen, split ? static_cast<int32_t>(slots) : -1,
+          split ? good.pieces : 2}},
+    };
+    for (const auto& b : bad) {
+      std::vector<t2v::Item> copy = items;
+      copy[i] = b.second;
+      const std::string why =
+          t2v::check_work_items(copy.data(), n, own.data(), loop.data(), nseq, heads, block, slots, false);
+      CHECK(why.find(b.first) != std::string::npos, ("corrupted item reported: " + std::string(b.first)).c_str());
+      ++corrupted;
+    }
+    if (!red.empty()) {
+      std::vector<t2v::Item> copy = red;
+      copy.back().pieces += 1;  // one slot past the last
+      CHECK(t2v::check_work_items(copy.data(), static_cast<int>(copy.size()), own.data(), loop.data(), nseq, heads,
+                                  block, slots, true).find("partial slots") != std::string::npos,
+            "reduce item past the slots reported");
+    }
+  }
+  std::printf("work-item checks: %d corrupted lists reported\n", corrupted);
+}
+
 int main() {
   std::mt19937 rng(20260);
+  work_item_checks(rng);
   range_allocator(rng);
   worklists(rng);
   loop_split(rng);

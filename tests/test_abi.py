@@ -34,6 +34,13 @@ def test_hip_library_exports_every_symbol():
     assert "gfx950" in _lib.t2v_version(L)
 
 
+def test_checked_library_exports_every_symbol():
+    L = _lib.checked_lib()
+    for n in declared_functions():
+        assert hasattr(L, n), n
+    assert "gfx950" in _lib.t2v_version(L)
+
+
 def test_host_library_exports():
     L = _lib.host_lib()
     for n in _lib.HOST_EXPORTS:
@@ -126,6 +133,20 @@ def test_bwd_validation(kw, msg):
 def test_bwd_empty_is_ok():
     st, _ = bwd([0, 0], q=0, k=0, v=0, out=0, lse=0, dout=0, dq=0, dk=0, dv=0, delta=0)
     assert st == _lib.T2V_OK
+
+
+def test_checked_library_validates_before_any_device_call():
+    """The checked library refuses bad arguments like the product library, and returns T2V_OK
+    for an empty pack, without a device call: its checks start at a call's first launch."""
+    with _lib.use_checked_library():
+        st, err = fwd([0, 5], heads=(1 << 15) + 1)
+        assert st == INV and "too large" in err
+        st, _ = fwd([0, 0, 0], q=0, k=0, v=0, out=0, lse=0)
+        assert st == _lib.T2V_OK
+        st, err = bwd([0, 7, 20], dout=0)
+        assert st == INV and "dout is NULL" in err
+        assert _lib.lib() is _lib.checked_lib()
+    assert _lib.lib() is not _lib.checked_lib()
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
@@ -247,7 +268,7 @@ int main(void) {
 """
 
 
-@pytest.mark.parametrize("lib", ["t2vattn_host", "t2vattn"])
+@pytest.mark.parametrize("lib", ["t2vattn_host", "t2vattn", "t2vattn_checked"])
 def test_header_is_plain_c_and_links(tmp_path, lib):
     """A C99 program that includes only the public header, built with -pedantic -Werror,
     links against the host-only and the GPU library and runs (no device work)."""
@@ -259,7 +280,7 @@ def test_header_is_plain_c_and_links(tmp_path, lib):
     src.write_text(C_CONSUMER)
     exe = str(tmp_path / "consumer")
     libdir = os.path.dirname(_lib.LIB_PATH)
-    gpu = ["-DWITH_GPU_LIBRARY"] if lib == "t2vattn" else []
+    gpu = ["-DWITH_GPU_LIBRARY"] if lib != "t2vattn_host" else []
     r = subprocess.run(["gcc", "-std=c99", "-Wall", "-Wextra", "-pedantic", "-Werror", *gpu, "-I",
                         os.path.join(ROOT, "include"), str(src), "-o", exe, f"-L{libdir}", f"-l{lib}",
                         f"-Wl,-rpath,{libdir}"], capture_output=True, text=True, timeout=120)
@@ -267,7 +288,7 @@ def test_header_is_plain_c_and_links(tmp_path, lib):
     r = subprocess.run([exe], capture_output=True, text=True, timeout=120)
     assert r.returncode == 0, (r.returncode, r.stdout, r.stderr)
     assert "libt2vattn" in r.stdout
-    assert ("NULL" if lib == "t2vattn" else "cu_seqlens") in r.stdout  # the refused call's message
+    assert ("NULL" if lib != "t2vattn_host" else "cu_seqlens") in r.stdout  # the refused call's message
 
 
 # ----------------------------------------------------------------- torch binding checks
