@@ -1309,6 +1309,8 @@ def main():
     res, pack = run_workload(args.workload, args.seed, args.steps, args.warmup)
     res["mfma_probe"] = mfma_probe()
     res["roofline"]["frac_of_probe"] = round(res["roofline"]["achieved"] / res["mfma_probe"]["tflops"], 4)
+    # The step against the MFMA ceiling measured on this GPU (context beside the published peak).
+    res["frac_of_probe_peak"] = round(res["value"] / res["mfma_probe"]["tflops"], 4)
     if args.workload == "hetero" and not args.no_extras:
         res["workloads"] = workloads_summary(args.seed, res)
         res["fresh_packs"] = fresh_pack_report(args.seed)
