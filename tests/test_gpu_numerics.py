@@ -72,12 +72,12 @@ def test_reference_moves_every_step(D):
     assert np.all(np.diff(step_max) > 8.0)
     errs, worst = compare_full(g, ref, pack.cu_seqlens, f"rising D={D}")
     # Near one-hot rows make dq a cancelling sum of dS times keys with a large shared part,
-    # so bf16 rounding of dS alone costs ~1% here; dq is held to 3x that floor (and never
-    # to less than the usual 2e-2), every other output to the usual bounds.
+    # so bf16 rounding of dS alone costs ~1% here (logged); every output, dq included, is
+    # still held to the usual bounds (measured dq 1.83e-2 at D = 128, 1.79e-2 at 64; the
+    # kernels are deterministic, so these inputs always give the same errors).
     floor = dq_error_of_bf16_ds(pack, ref)
     log(f"  dq error with only dS rounded to bf16: {floor:.3e}")
-    assert errs["dq"] <= max(2e-2, 3.0 * floor), (errs["dq"], floor)
-    errs["dq"] = 0.0
+    assert errs["dq"] >= 0.5 * floor, (errs["dq"], floor)  # the inputs do stress dq as intended
     assert_within(errs)
 
 
