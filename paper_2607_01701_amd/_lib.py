@@ -107,10 +107,11 @@ _route = threading.local()  # .checked: this thread's calls go to the checked li
 
 
 def lib():
-    """The HIP library (loaded once), or the checked library inside use_checked_library().
-    Raises if it has not been built."""
+    """The HIP library (loaded once), or the checked library inside use_checked_library() or
+    when the environment sets T2V_CHECKED=1 (to run a whole program against it). Raises if
+    it has not been built."""
     global _lib
-    if getattr(_route, "checked", False):
+    if getattr(_route, "checked", False) or os.environ.get("T2V_CHECKED") == "1":
         return checked_lib()
     if _lib is None:
         if not os.path.exists(LIB_PATH):
