@@ -8,3 +8,4 @@ from ._lib import (  # noqa: F401
     t2v_build_worklist, t2v_kernel_times, t2v_last_error, t2v_timing_enable, t2v_plan_makespan, t2v_release_cache, t2v_version,
     use_checked_library,
 )
+from .autograd import varlen_attention  # noqa: F401
