@@ -149,6 +149,22 @@ def test_checked_library_validates_before_any_device_call():
     assert _lib.lib() is not _lib.checked_lib()
 
 
+def test_checked_routing_is_per_thread_and_by_environment(monkeypatch):
+    """use_checked_library() routes only the calling thread; T2V_CHECKED=1 routes every call."""
+    import threading
+    seen = {}
+    with _lib.use_checked_library():
+        t = threading.Thread(target=lambda: seen.setdefault("other", _lib.lib()))
+        t.start()
+        t.join()
+        assert _lib.lib() is _lib.checked_lib()
+    assert seen["other"] is not _lib.checked_lib()
+    monkeypatch.setenv("T2V_CHECKED", "1")
+    assert _lib.lib() is _lib.checked_lib()
+    monkeypatch.delenv("T2V_CHECKED")
+    assert _lib.lib() is not _lib.checked_lib()
+
+
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(_lib, "_lib", None)
     monkeypatch.setattr(_lib, "LIB_PATH", str(tmp_path / "missing.so"))
